@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Throughput of the fused local update + P-Reduce step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config C]
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+the host group schedule for step t, then one launch of the fused kernel that
+applies every active worker's local update and the P-Reduce of every group.
+The default workload is 16 fp32 replicas of a 25.6M-parameter (ResNet-50
+sized) model with a seeded static schedule of four groups of four (the
+configuration the headline metric is quoted on).
+
+Prints one JSON line (stdout).  ``value`` is algorithmic HBM bytes of the K
+timed steps divided by their wall time, inputs resident in HBM before timing
+starts.  ``roofline.achieved`` is the algorithmic bytes of one launch over the
+kernel's mean duration measured with HIP events on its stream.
+``cpu_baseline`` times the CPU oracle on a bounded sample of the same
+workload.  Progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "P-Reduce+update effective HBM GB/s and % of MI355X HBM peak"
+KERNEL_SOURCES = ["paper_1909_08029_amd/csrc/rip_kernels.hip",
+                  "paper_1909_08029_amd/csrc/rip_kernel_args.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def err(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM bytes per launch measured with rocprofv3 counters, if they were
+    taken on the current kernel source for this workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = data.get(workload)
+    if not ent or ent.get("kernel_hash") != kernel_hash():
+        return None
+    return ent.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(w, seconds: float = 12.0):
+    """The oracle as it stands, single-threaded numpy, on one window of every
+    replica, for as many steps of the workload's schedule as fit the budget
+    (at least 2).  Times the update + group averaging only."""
+    import numpy as np
+    from oracle import preduce as op
+    from oracle import sched as osd
+    from seedgen import DTYPE_BF16
+    from seedgen import workloads as wl
+
+    width = min(w.numel, 1 << 22)
+    a, b = 0, width
+    kw = dict(w.sched)
+    mode = kw.pop("mode")
+    sch = osd.Scheduler(w.n, mode, **kw)
+    p, grad, v = wl.host_inputs(w, a, b)
+    dt = op.BF16 if w.dtype == DTYPE_BF16 else op.F32
+    sub = wl.scaled(w, [width])
+    spent, nbytes, steps = 0.0, 0, 0
+    while steps < 2 or (spent < seconds and steps < w.steps):
+        active, groups = sch.step(steps, w.eligible(steps))
+        g = grad(w.grad_slot(steps))
+        t0 = time.perf_counter()
+        p, v = op.step(p, g, v, groups, active, w.lr, w.momentum or None, dt)
+        spent += time.perf_counter() - t0
+        nbytes += sub.alg_bytes(active, groups)
+        steps += 1
+    return dict(value=round(nbytes / spent / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
+                sample=f"{steps} steps of the workload schedule on elements [0, {width}) of all "
+                       f"{w.n} replicas ({100.0 * width / w.numel:.1f}% of each replica), "
+                       f"numpy single-threaded, host has {os.cpu_count()} CPUs; "
+                       f"{spent:.1f} s timed, update+average only")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--layout", default="flat", choices=["flat", "separate"])
+    ap.add_argument("--grad-ring", type=int, default=None)
+    ap.add_argument("--max-blocks", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: every replica of the P-Reduce path lives in one "
+              "MI355X's HBM and this build has no multi-GPU path; run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1909_08029_amd as rip
+    from seedgen import DTYPE_BF16
+    from seedgen import workloads as wl
+
+    if not torch.cuda.is_available():
+        err("no GPU visible")
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    w = wl.CONFIGS[args.config]
+    if args.grad_ring:
+        w = wl.scaled(w, w.seg_numel, grad_ring=args.grad_ring)
+    err(f"[bench] workload {w.name}: N={w.n} P={w.numel} layout={args.layout}")
+    if args.max_blocks:
+        rip.rip_set_max_blocks(args.max_blocks)
+
+    st = wl.DeviceState(w, args.layout)
+    st.fill()
+    handles = [rip.Replicas(st.param, gs, st.mom) for gs in st.grad_sets]
+    sched_kw = dict(w.sched)
+    sched = rip.Scheduler(w.n, sched_kw.pop("mode"), **sched_kw)
+    torch.cuda.synchronize()
+    err("[bench] inputs resident")
+
+    stream = torch.cuda.current_stream()
+    t = 0
+
+    def one_step(ev=None):
+        nonlocal t
+        active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
+        h = handles[w.grad_slot(t)]
+        if ev is not None:
+            ev[0].record(stream)
+        rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        t += 1
+        return w.alg_bytes(active, groups)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    err(f"[bench] {args.warmup} warmup steps done")
+
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    total_bytes = 0
+    per_step_bytes = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        b = one_step(events[i])
+        per_step_bytes.append(b)
+        total_bytes += b
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [s.elapsed_time(e) for s, e in events]
+    launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
+    err(f"[bench] {args.steps} timed steps: {wall * 1e3:.2f} ms wall")
+
+    # host scheduling cost alone (fresh scheduler, same steps)
+    sched_kw = dict(w.sched)
+    sch2 = rip.Scheduler(w.n, sched_kw.pop("mode"), **sched_kw)
+    h0 = time.perf_counter()
+    for i in range(args.steps):
+        rip.rip_schedule_groups(sch2, i, w.eligible(i))
+    sched_us = (time.perf_counter() - h0) / args.steps * 1e6
+
+    value = total_bytes / wall / 1e9
+    mean_launch_bytes = sum(b for b, _ in launched) / max(1, len(launched))
+    mean_kernel_ms = sum(ms for _, ms in launched) / max(1, len(launched))
+    achieved = mean_launch_bytes / (mean_kernel_ms * 1e-3) / 1e9 if launched else 0.0
+    traffic = load_traffic(w.name + ("" if args.layout == "flat" else "_separate"))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        err("[bench] timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(w)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "n_replicas": w.n,
+            "params_per_replica": w.numel,
+            "segments": len(w.seg_numel),
+            "layout": args.layout,
+            "storage": "bf16" if w.dtype == DTYPE_BF16 else "fp32",
+            "optimizer": f"sgd lr={w.lr}" + (f" momentum={w.momentum}" if w.momentum else ""),
+            "schedule": w.sched.get("mode"),
+            "grad_ring": w.grad_ring,
+            "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
+            "host_schedule_us_per_step": round(sched_us, 2),
+            "parallelism": "single-gpu",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "alg_bytes_per_launch": int(mean_launch_bytes),
+            "mean_kernel_us": round(mean_kernel_ms * 1e3, 2),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

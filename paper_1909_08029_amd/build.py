@@ -1,0 +1,57 @@
+"""Build librip.so (the P-Reduce library) and libseedgen.so (input generator)
+in-tree with hipcc for gfx950.
+
+    python -m paper_1909_08029_amd.build        # or __graft_entry__.build()
+
+Always recompiles.  Flags: -O3, fp contraction off (the kernels' arithmetic
+order is part of their contract), packed-fp32 instructions disabled.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+COMMON = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "-ffp-contract=off", "-Wall",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+]
+
+LIBRIP = os.path.join(PKG, "librip.so")
+LIBSEEDGEN = os.path.join(ROOT, "seedgen", "libseedgen.so")
+
+
+def _run(cmd):
+    print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+
+
+def build_librip(out: str = LIBRIP, extra=()):
+    csrc = os.path.join(PKG, "csrc")
+    srcs = [os.path.join(csrc, f) for f in ("rip_api.hip", "rip_kernels.hip", "rip_sched.cpp")]
+    tmp = out + ".tmp"
+    _run([HIPCC, *COMMON, *extra, "-I", os.path.join(ROOT, "include"), "-I", csrc,
+          "-x", "hip", *srcs, "-o", tmp])
+    os.replace(tmp, out)
+
+
+def build_seedgen(out: str = LIBSEEDGEN):
+    tmp = out + ".tmp"
+    _run([HIPCC, *COMMON, os.path.join(ROOT, "seedgen", "csrc", "seedgen.hip"), "-o", tmp])
+    os.replace(tmp, out)
+
+
+def build_all():
+    build_librip()
+    build_seedgen()
+
+
+if __name__ == "__main__":
+    build_all()
+    sys.exit(0)

@@ -1,0 +1,287 @@
+// Host side of librip: replica registration, argument checking, building the
+// per-step launch descriptor, and error reporting.  The contract of every
+// entry point is in include/rip.h.
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "rip_internal.h"
+#include "rip_kernel_args.h"
+
+namespace rip {
+
+namespace {
+thread_local std::string g_last_error;
+std::atomic<int> g_max_blocks{0};
+constexpr int kDefaultMaxBlocks = 1 << 20;
+}  // namespace
+
+int32_t fail(int32_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+}  // namespace rip
+
+struct rip_replicas {
+  int32_t n = 0, n_seg = 0, dtype = 0, device = 0;
+  bool has_grad = false, has_mom = false;
+  int64_t tiles = 0;
+  void* dmem = nullptr;  // ptab [3][S][N] u64 | seg_numel [S] i64 | seg_tile0 [S+1] i64
+  const uint64_t* d_ptab = nullptr;
+  const int64_t* d_numel = nullptr;
+  const int64_t* d_tile0 = nullptr;
+};
+
+extern "C" const char* rip_last_error(void) { return rip::g_last_error.c_str(); }
+extern "C" int32_t rip_abi_version(void) { return RIP_ABI_VERSION; }
+
+extern "C" int32_t rip_set_max_blocks(int32_t max_blocks) {
+  if (max_blocks < 0) return rip::fail(RIP_E_INVAL, "max_blocks must be >= 0");
+  rip::g_max_blocks.store(max_blocks);
+  return RIP_OK;
+}
+
+namespace {
+
+int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
+int elem_size(int32_t dtype) { return dtype == RIP_BF16 ? 2 : 4; }
+
+// True when, for every replica, segment s+1 starts right after segment s in
+// memory (for one pointer kind).
+bool back_to_back(void* const* p, int32_t n, int32_t S, const int64_t* numel, int esize) {
+  for (int32_t r = 0; r < n; ++r)
+    for (int32_t s = 0; s + 1 < S; ++s) {
+      const char* a = static_cast<const char*>(p[(size_t)r * S + s]);
+      const char* b = static_cast<const char*>(p[(size_t)r * S + s + 1]);
+      if (numel[s] == 0 || numel[s + 1] == 0) return false;
+      if (a + numel[s] * esize != b) return false;
+    }
+  return true;
+}
+
+int32_t check_ptrs(void* const* p, const char* what, int32_t n, int32_t S, const int64_t* numel) {
+  for (int32_t r = 0; r < n; ++r)
+    for (int32_t s = 0; s < S; ++s) {
+      const void* q = p[(size_t)r * S + s];
+      if (numel[s] == 0) continue;
+      if (!q) return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] is NULL", what, r, s);
+      if (reinterpret_cast<uintptr_t>(q) % 16 != 0)
+        return rip::fail(RIP_E_ALIGN, "%s[%d*S+%d] = %p is not 16-byte aligned", what, r, s, q);
+    }
+  return RIP_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, int32_t dtype,
+                                       const int64_t* seg_numel, void* const* param,
+                                       void* const* grad, void* const* mom, rip_replicas** out) {
+  rip::clear_error();
+  if (!out) return rip::fail(RIP_E_INVAL, "rip_replicas_create: out is NULL");
+  *out = nullptr;
+  if (dtype != RIP_FP32 && dtype != RIP_BF16)
+    return rip::fail(RIP_E_UNSUPPORTED, "unknown dtype %d", dtype);
+  if (n_replicas < 1) return rip::fail(RIP_E_INVAL, "n_replicas %d < 1", n_replicas);
+  if (n_replicas > RIP_MAX_REPLICAS)
+    return rip::fail(RIP_E_UNSUPPORTED, "n_replicas %d > %d", n_replicas, RIP_MAX_REPLICAS);
+  if (n_segments < 1 || !seg_numel || !param)
+    return rip::fail(RIP_E_INVAL, "need n_segments >= 1, seg_numel and param");
+  for (int32_t s = 0; s < n_segments; ++s)
+    if (seg_numel[s] < 0) return rip::fail(RIP_E_INVAL, "seg_numel[%d] < 0", s);
+  int32_t rc;
+  if ((rc = check_ptrs(param, "param", n_replicas, n_segments, seg_numel)) != RIP_OK) return rc;
+  if (grad && (rc = check_ptrs(grad, "grad", n_replicas, n_segments, seg_numel)) != RIP_OK)
+    return rc;
+  if (mom && (rc = check_ptrs(mom, "mom", n_replicas, n_segments, seg_numel)) != RIP_OK)
+    return rc;
+
+  // Collapse back-to-back segments into one flat range per replica.
+  const int esize = elem_size(dtype);
+  int64_t total = 0;
+  for (int32_t s = 0; s < n_segments; ++s) total += seg_numel[s];
+  const bool flat = n_segments == 1 ||
+                    (back_to_back(param, n_replicas, n_segments, seg_numel, esize) &&
+                     (!grad || back_to_back(grad, n_replicas, n_segments, seg_numel, esize)) &&
+                     (!mom || back_to_back(mom, n_replicas, n_segments, seg_numel, esize)));
+  const int32_t S = flat ? 1 : n_segments;
+  const int32_t N = n_replicas;
+  std::vector<uint64_t> ptab((size_t)3 * S * N, 0);
+  std::vector<int64_t> numel(S), tile0(S + 1);
+  const int64_t tile_elems = (int64_t)rip::kBlock * rip::kSlots * elems_per_16b(dtype);
+  for (int32_t s = 0; s < S; ++s) {
+    numel[s] = flat ? total : seg_numel[s];
+    tile0[s] = s == 0 ? 0 : tile0[s - 1] + (numel[s - 1] + tile_elems - 1) / tile_elems;
+    for (int32_t r = 0; r < N; ++r) {
+      const size_t src = (size_t)r * n_segments + s;
+      const size_t dst = (size_t)s * N + r;
+      ptab[dst] = reinterpret_cast<uint64_t>(param[src]);
+      ptab[(size_t)S * N + dst] = grad ? reinterpret_cast<uint64_t>(grad[src]) : 0;
+      ptab[(size_t)2 * S * N + dst] = mom ? reinterpret_cast<uint64_t>(mom[src]) : 0;
+    }
+  }
+  tile0[S] = tile0[S - 1] + (numel[S - 1] + tile_elems - 1) / tile_elems;
+
+  rip_replicas* h = new (std::nothrow) rip_replicas();
+  if (!h) return rip::fail(RIP_E_NOMEM, "out of host memory");
+  h->n = N;
+  h->n_seg = S;
+  h->dtype = dtype;
+  h->has_grad = grad != nullptr;
+  h->has_mom = mom != nullptr;
+  h->tiles = tile0[S];
+  hipError_t e = hipGetDevice(&h->device);
+  const size_t bytes_ptab = ptab.size() * sizeof(uint64_t);
+  const size_t bytes = bytes_ptab + (size_t)S * 8 + (size_t)(S + 1) * 8;
+  if (e == hipSuccess) e = hipMalloc(&h->dmem, bytes);
+  if (e != hipSuccess) {
+    delete h;
+    return rip::fail(e == hipErrorOutOfMemory ? RIP_E_NOMEM : RIP_E_HIP,
+                     "rip_replicas_create: %s", hipGetErrorString(e));
+  }
+  char* d = static_cast<char*>(h->dmem);
+  std::vector<char> staging(bytes);
+  std::memcpy(staging.data(), ptab.data(), bytes_ptab);
+  std::memcpy(staging.data() + bytes_ptab, numel.data(), (size_t)S * 8);
+  std::memcpy(staging.data() + bytes_ptab + (size_t)S * 8, tile0.data(), (size_t)(S + 1) * 8);
+  e = hipMemcpy(d, staging.data(), bytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(h->dmem);
+    delete h;
+    return rip::fail(RIP_E_HIP, "rip_replicas_create: %s", hipGetErrorString(e));
+  }
+  h->d_ptab = reinterpret_cast<const uint64_t*>(d);
+  h->d_numel = reinterpret_cast<const int64_t*>(d + bytes_ptab);
+  h->d_tile0 = reinterpret_cast<const int64_t*>(d + bytes_ptab + (size_t)S * 8);
+  *out = h;
+  return RIP_OK;
+}
+
+extern "C" void rip_replicas_destroy(rip_replicas* r) {
+  if (!r) return;
+  if (r->dmem) (void)hipFree(r->dmem);
+  delete r;
+}
+
+namespace {
+
+// Checks one step's schedule and turns it into units (groups first, in the
+// order given, then active workers outside every group, ascending).
+int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const int32_t* members,
+                   int32_t n_groups, const int32_t* active, int32_t n_active, const rip_sgd* sgd,
+                   rip::StepArgs& a) {
+  const int32_t N = r->n;
+  if (n_groups < 0 || n_active < 0) return rip::fail(RIP_E_INVAL, "negative count");
+  if (n_groups > 0 && (!group_offsets || !members))
+    return rip::fail(RIP_E_INVAL, "groups given without group_offsets/members");
+  if (n_active > 0 && !active) return rip::fail(RIP_E_INVAL, "active is NULL");
+  if (!sgd && n_active > 0) return rip::fail(RIP_E_INVAL, "active workers need an sgd step");
+  if (n_active > N) return rip::fail(RIP_E_INVAL, "n_active %d > n_replicas %d", n_active, N);
+  if (sgd && n_active > 0) {
+    if (!r->has_grad) return rip::fail(RIP_E_INVAL, "local update without gradient buffers");
+    if (sgd->momentum != 0.0f && !r->has_mom)
+      return rip::fail(RIP_E_INVAL, "momentum %g without momentum buffers", (double)sgd->momentum);
+  }
+  std::vector<uint8_t> in_group(N, 0), is_active(N, 0);
+  for (int32_t i = 0; i < n_active; ++i) {
+    const int32_t id = active[i];
+    if (id < 0 || id >= N) return rip::fail(RIP_E_INVAL, "active id %d out of range", id);
+    if (is_active[id]) return rip::fail(RIP_E_INVAL, "active id %d listed twice", id);
+    is_active[id] = 1;
+  }
+  if (n_groups > 0 && group_offsets[0] != 0)
+    return rip::fail(RIP_E_INVAL, "group_offsets[0] must be 0");
+  for (int32_t g = 0; g < n_groups; ++g) {
+    const int32_t b = group_offsets[g], e = group_offsets[g + 1];
+    if (e <= b) return rip::fail(RIP_E_INVAL, "group %d is empty or offsets decrease", g);
+    if (e > N) return rip::fail(RIP_E_OVERLAP, "groups list more than %d members", N);
+    for (int32_t j = b; j < e; ++j) {
+      const int32_t m = members[j];
+      if (m < 0 || m >= N) return rip::fail(RIP_E_INVAL, "member %d of group %d out of range", m, g);
+      if (j > b && m <= members[j - 1])
+        return rip::fail(RIP_E_INVAL, "group %d is not strictly ascending", g);
+      if (in_group[m]) return rip::fail(RIP_E_OVERLAP, "replica %d is in two groups", m);
+      in_group[m] = 1;
+    }
+  }
+
+  std::memset(&a, 0, sizeof a);
+  int32_t units = 0, pos = 0;
+  a.unit_off[0] = 0;
+  for (int32_t g = 0; g < n_groups; ++g) {
+    const int32_t b = group_offsets[g], e = group_offsets[g + 1];
+    if (e - b == 1 && !is_active[members[b]]) continue;  // identity: nothing to do
+    for (int32_t j = b; j < e; ++j) a.member[pos++] = (uint16_t)members[j];
+    a.unit_off[++units] = (uint16_t)pos;
+  }
+  for (int32_t id = 0; id < N; ++id)
+    if (is_active[id] && !in_group[id]) {
+      a.member[pos++] = (uint16_t)id;
+      a.unit_off[++units] = (uint16_t)pos;
+    }
+  for (int32_t id = 0; id < N; ++id)
+    if (is_active[id]) a.active_bits[id >> 5] |= 1u << (id & 31);
+  a.ptab = r->d_ptab;
+  a.seg_numel = r->d_numel;
+  a.seg_tile0 = r->d_tile0;
+  a.tiles = r->tiles;
+  a.work = (int64_t)units * r->tiles;
+  if (a.work >= (int64_t)1 << 31)
+    return rip::fail(RIP_E_UNSUPPORTED, "%lld work items exceed 2^31 (segments too large)",
+                     (long long)a.work);
+  a.n_seg = r->n_seg;
+  a.n_rep = N;
+  a.n_units = units;
+  a.lr = sgd ? sgd->lr : 0.0f;
+  a.mu = sgd ? sgd->momentum : 0.0f;
+  return RIP_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offsets,
+                               const int32_t* members, int32_t n_groups, const int32_t* active,
+                               int32_t n_active, const rip_sgd* sgd, void* stream) {
+  rip::clear_error();
+  if (!r) return rip::fail(RIP_E_INVAL, "rip_preduce: replicas handle is NULL");
+  rip::StepArgs a;
+  int32_t rc = build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a);
+  if (rc != RIP_OK) return rc;
+  if (a.work == 0) return RIP_OK;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return rip::fail(RIP_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev != r->device)
+    return rip::fail(RIP_E_INVAL, "current device %d differs from the handle's device %d", dev,
+                     r->device);
+  const int cap = rip::g_max_blocks.load() > 0 ? rip::g_max_blocks.load() : rip::kDefaultMaxBlocks;
+  const int blocks = (int)(a.work < cap ? a.work : cap);
+  const bool mom = a.mu != 0.0f && n_active > 0;
+  e = rip::launch_fused_step(a, r->dtype == RIP_BF16, mom, blocks,
+                             static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return rip::fail(RIP_E_HIP, "kernel launch: %s", hipGetErrorString(e));
+  return RIP_OK;
+}
+
+extern "C" int32_t rip_local_step(const rip_replicas* r, const int32_t* active, int32_t n_active,
+                                  const rip_sgd* sgd, void* stream) {
+  if (!sgd) {
+    rip::clear_error();
+    return rip::fail(RIP_E_INVAL, "rip_local_step: sgd is NULL");
+  }
+  return rip_preduce(r, nullptr, nullptr, 0, active, n_active, sgd, stream);
+}

@@ -1,0 +1,310 @@
+// Fused local update + P-Reduce for CDNA4 (gfx950).
+//
+// One launch runs one step of the algorithm of Fig. 4 for every scheduled
+// unit of work: a group G (Step 4, the F^G of Sec. 3.2, with the Step 2
+// update of its members that compute this step folded in) or a worker that
+// updates without synchronizing.  Disjoint groups run concurrently (Sec. 3.2).
+//
+// Work decomposition.  Every unit touches the same element range of its
+// members' buffers, so the launch is a grid of (unit, tile) work items; a
+// tile is 256 threads x 4 slots x 16 bytes of each member stream.  A
+// workgroup handles one unit at a time, so the unit's size k, its member ids
+// and their active flags are wave-uniform: they sit in scalar registers and
+// every branch on them is a scalar branch.  Each thread keeps the loads of
+// all k members (and their gradients / momenta) of one or more 16-byte slots
+// in flight before any arithmetic, then writes the mean back to every member.
+//
+// The operation is a stream over HBM with no data reuse and about one flop
+// per 4 bytes, so there is no LDS tiling and no matrix-core work: the design
+// aims at full-width (dwordx4) coalesced accesses and enough bytes in flight
+// per CU.
+//
+// Arithmetic follows the exact fp32 order documented in include/rip.h (no
+// contraction into FMA, sequential sum in ascending member order, product
+// with (float)(1.0/k)); bf16 values widen exactly and round to nearest-even
+// once when stored.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "rip_kernel_args.h"
+
+#pragma clang fp contract(off)
+
+namespace rip {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Replica buffers are plain device memory: access them through the global
+// address space so the compiler emits global_* (not flat_*) instructions.
+#define RIP_GLOBAL __attribute__((address_space(1)))
+
+__device__ __forceinline__ u32x4 ld16(const char* p) {
+  return __builtin_nontemporal_load((const RIP_GLOBAL u32x4*)p);
+}
+__device__ __forceinline__ void st16(char* p, u32x4 v) {
+  __builtin_nontemporal_store(v, (RIP_GLOBAL u32x4*)p);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xFFFF0000u); }
+
+// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t bf16_round(float f) {
+  const uint32_t b = __float_as_uint(f);
+  const uint32_t r = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+  return ((b & 0x7FFFFFFFu) > 0x7F800000u) ? ((b >> 16) | 0x40u) : r;
+}
+
+template <bool BF16>
+struct Vec;
+
+// 16 bytes = 4 fp32
+template <>
+struct Vec<false> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void unpack(u32x4 x, float (&f)[N]) {
+    f[0] = __uint_as_float(x.x);
+    f[1] = __uint_as_float(x.y);
+    f[2] = __uint_as_float(x.z);
+    f[3] = __uint_as_float(x.w);
+  }
+  static __device__ __forceinline__ u32x4 pack(const float (&f)[N]) {
+    u32x4 x;
+    x.x = __float_as_uint(f[0]);
+    x.y = __float_as_uint(f[1]);
+    x.z = __float_as_uint(f[2]);
+    x.w = __float_as_uint(f[3]);
+    return x;
+  }
+};
+
+// 16 bytes = 8 bf16; element 2i is the low half of word i
+template <>
+struct Vec<true> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void unpack(u32x4 x, float (&f)[N]) {
+    f[0] = bf16_lo(x.x); f[1] = bf16_hi(x.x);
+    f[2] = bf16_lo(x.y); f[3] = bf16_hi(x.y);
+    f[4] = bf16_lo(x.z); f[5] = bf16_hi(x.z);
+    f[6] = bf16_lo(x.w); f[7] = bf16_hi(x.w);
+  }
+  static __device__ __forceinline__ u32x4 pack(const float (&f)[N]) {
+    u32x4 x;
+    x.x = bf16_round(f[0]) | (bf16_round(f[1]) << 16);
+    x.y = bf16_round(f[2]) | (bf16_round(f[3]) << 16);
+    x.z = bf16_round(f[4]) | (bf16_round(f[5]) << 16);
+    x.w = bf16_round(f[6]) | (bf16_round(f[7]) << 16);
+    return x;
+  }
+};
+
+// Scalar element access for tails and the generic (k > 8) path.
+template <bool BF16>
+__device__ __forceinline__ float ld1(const char* base, int64_t e) {
+  if constexpr (BF16)
+    return __uint_as_float(uint32_t(((const RIP_GLOBAL uint16_t*)base)[e]) << 16);
+  else
+    return ((const RIP_GLOBAL float*)base)[e];
+}
+template <bool BF16>
+__device__ __forceinline__ void st1(char* base, int64_t e, float v) {
+  if constexpr (BF16)
+    ((RIP_GLOBAL uint16_t*)base)[e] = (uint16_t)bf16_round(v);
+  else
+    ((RIP_GLOBAL float*)base)[e] = v;
+}
+
+// (float)(1.0/k) for every group size, evaluated at compile time.
+struct InvTable {
+  float v[RIP_MAX_REPLICAS + 1];
+};
+constexpr InvTable make_inv_table() {
+  InvTable t{};
+  for (int k = 1; k <= RIP_MAX_REPLICAS; ++k) t.v[k] = (float)(1.0 / k);
+  return t;
+}
+__constant__ InvTable kInv = make_inv_table();
+
+struct Members {
+  char* w[kMaxK];
+  const char* g[kMaxK];
+  char* v[kMaxK];
+  bool act[kMaxK];
+};
+
+template <int K>
+__device__ __forceinline__ void load_members(const StepArgs& a, int base, int seg, Members& m) {
+  const int plane = a.n_seg * a.n_rep;
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const int id = a.member[base + j];
+    const int idx = seg * a.n_rep + id;
+    m.w[j] = reinterpret_cast<char*>(a.ptab[idx]);
+    m.g[j] = reinterpret_cast<const char*>(a.ptab[plane + idx]);
+    m.v[j] = reinterpret_cast<char*>(a.ptab[2 * plane + idx]);
+    m.act[j] = (a.active_bits[id >> 5] >> (id & 31)) & 1u;
+  }
+}
+
+// U consecutive 16-byte slots of a full tile for a unit of K members.
+template <int K, int U, bool BF16, bool MOM>
+__device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off)[U], float lr,
+                                           float mu) {
+  using V = Vec<BF16>;
+  constexpr int N = V::N;
+  constexpr float inv_k = (float)(1.0 / K);
+  u32x4 wv[U][K], gv[U][K], vv[U][K];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      wv[u][j] = ld16(m.w[j] + off[u]);
+      if (m.act[j]) {
+        gv[u][j] = ld16(m.g[j] + off[u]);
+        if constexpr (MOM) vv[u][j] = ld16(m.v[j] + off[u]);
+      }
+    }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float s[N];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      float x[N];
+      V::unpack(wv[u][j], x);
+      if (m.act[j]) {
+        float g[N];
+        V::unpack(gv[u][j], g);
+        if constexpr (MOM) {
+          float v[N];
+          V::unpack(vv[u][j], v);
+#pragma unroll
+          for (int i = 0; i < N; ++i) {
+            v[i] = mu * v[i] + g[i];
+            x[i] = x[i] - lr * v[i];
+          }
+          st16(m.v[j] + off[u], V::pack(v));
+        } else {
+#pragma unroll
+          for (int i = 0; i < N; ++i) x[i] = x[i] - lr * g[i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < N; ++i) s[i] = (j == 0) ? x[i] : s[i] + x[i];
+    }
+    if constexpr (K > 1) {
+#pragma unroll
+      for (int i = 0; i < N; ++i) s[i] = s[i] * inv_k;
+    }
+    const u32x4 out = V::pack(s);
+#pragma unroll
+    for (int j = 0; j < K; ++j) st16(m.w[j] + off[u], out);
+  }
+}
+
+// Element-wise path for a partial tile or any k: each thread walks elements
+// e0 + i*stride below `end`.
+template <bool BF16, bool MOM>
+__device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t begin,
+                            int64_t end) {
+  const int plane = a.n_seg * a.n_rep;
+  const float inv_k = kInv.v[k];
+  for (int64_t e = begin + threadIdx.x; e < end; e += kBlock) {
+    float s = 0.0f;
+    for (int j = 0; j < k; ++j) {
+      const int id = a.member[base + j];
+      const int idx = seg * a.n_rep + id;
+      char* w = reinterpret_cast<char*>(a.ptab[idx]);
+      float x = ld1<BF16>(w, e);
+      if ((a.active_bits[id >> 5] >> (id & 31)) & 1u) {
+        const float g = ld1<BF16>(reinterpret_cast<const char*>(a.ptab[plane + idx]), e);
+        if constexpr (MOM) {
+          char* vp = reinterpret_cast<char*>(a.ptab[2 * plane + idx]);
+          const float v = a.mu * ld1<BF16>(vp, e) + g;
+          st1<BF16>(vp, e, v);
+          x = x - a.lr * v;
+        } else {
+          x = x - a.lr * g;
+        }
+      }
+      s = (j == 0) ? x : s + x;
+    }
+    if (k > 1) s = s * inv_k;
+    for (int j = 0; j < k; ++j) {
+      const int id = a.member[base + j];
+      st1<BF16>(reinterpret_cast<char*>(a.ptab[seg * a.n_rep + id]), e, s);
+    }
+  }
+}
+
+template <int K, bool BF16, bool MOM>
+__device__ __forceinline__ void full_tile(const StepArgs& a, int base, int seg, int64_t e_tile) {
+  constexpr int U = (K <= 2) ? 4 : (K <= 4 ? 2 : 1);
+  constexpr int N = Vec<BF16>::N;
+  constexpr int esize = BF16 ? 2 : 4;
+  Members m;
+  load_members<K>(a, base, seg, m);
+#pragma unroll
+  for (int s0 = 0; s0 < kSlots; s0 += U) {
+    int64_t off[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      off[u] = (e_tile + (int64_t)((s0 + u) * kBlock + (int)threadIdx.x) * N) * esize;
+    tile_slots<K, U, BF16, MOM>(m, off, a.lr, a.mu);
+  }
+}
+
+template <bool BF16, bool MOM>
+__global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
+  constexpr int64_t tile_elems = (int64_t)kBlock * kSlots * Vec<BF16>::N;
+  const uint32_t tiles = (uint32_t)a.tiles;
+  for (uint32_t w = blockIdx.x; w < (uint32_t)a.work; w += gridDim.x) {
+    const int unit = (int)(w / tiles);
+    const int64_t tile = (int64_t)(w - (uint32_t)unit * tiles);
+    // segment holding this tile: the last s with seg_tile0[s] <= tile
+    int lo = 0, hi = a.n_seg - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.seg_tile0[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    const int seg = lo;
+    const int64_t e_tile = (tile - a.seg_tile0[seg]) * tile_elems;
+    const int64_t numel = a.seg_numel[seg];
+    const int base = a.unit_off[unit];
+    const int k = a.unit_off[unit + 1] - base;
+    if (e_tile + tile_elems <= numel) {
+      switch (k) {
+        case 1: full_tile<1, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 2: full_tile<2, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 3: full_tile<3, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 4: full_tile<4, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 5: full_tile<5, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 6: full_tile<6, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 7: full_tile<7, BF16, MOM>(a, base, seg, e_tile); continue;
+        case 8: full_tile<8, BF16, MOM>(a, base, seg, e_tile); continue;
+        default: break;
+      }
+    }
+    const int64_t end = (e_tile + tile_elems < numel) ? e_tile + tile_elems : numel;
+    elementwise<BF16, MOM>(a, base, k, seg, e_tile, end);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, int blocks,
+                             hipStream_t stream) {
+  const dim3 grid(blocks), block(kBlock);
+  if (bf16) {
+    if (mom) hipLaunchKernelGGL((fused_step_kernel<true, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((fused_step_kernel<true, false>), grid, block, 0, stream, a);
+  } else {
+    if (mom) hipLaunchKernelGGL((fused_step_kernel<false, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((fused_step_kernel<false, false>), grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace rip
