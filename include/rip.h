@@ -175,9 +175,10 @@ int32_t rip_sched_worker(const rip_sched* s, int32_t worker, rip_worker_state* o
  *  param  [N*S] host array of device pointers, param[r*S + s]
  *  grad   [N*S] or NULL (then only pure P-Reduce is possible)
  *  mom    [N*S] or NULL (momentum buffers, same storage type)
- * Every pointer must be 16-byte aligned; zero-length segments may be NULL.
- * When every replica's segments are laid out back to back in memory (and
- * likewise for grad and mom), they are treated as one flat segment.
+ * When every replica's non-empty segments lie back to back in memory (and
+ * likewise for grad and mom), they are treated as one flat range and only
+ * its first segment must be 16-byte aligned; otherwise every non-empty
+ * segment must be.  Zero-length segments may be NULL.
  * The handle copies the pointer table to device memory (one allocation,
  * freed by rip_replicas_destroy) on the current device; calls using it must
  * run with that device current.  Destroy only after the work that uses it

@@ -65,6 +65,10 @@ class Sgd(ctypes.Structure):
 
 
 def _load():
+    # torch ships its own HIP runtime.  Importing it first makes librip bind
+    # to that same runtime (the soname matches); loading librip first would
+    # pull in a second HIP runtime from /opt/rocm and the two do not mix.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                           "(there is no CPU fallback)")

@@ -29,7 +29,13 @@ LIBSEEDGEN = os.path.join(ROOT, "seedgen", "libseedgen.so")
 
 def _run(cmd):
     print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    # hipcc's host pass does not know the (device-only) packed-fp32 feature
+    out = "\n".join(l for l in res.stdout.splitlines() if "packed-fp32-ops" not in l)
+    if out.strip():
+        print(out, flush=True)
+    if res.returncode != 0:
+        raise subprocess.CalledProcessError(res.returncode, cmd)
 
 
 def build_librip(out: str = LIBRIP, extra=()):

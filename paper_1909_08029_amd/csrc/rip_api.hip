@@ -61,27 +61,41 @@ namespace {
 int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
 int elem_size(int32_t dtype) { return dtype == RIP_BF16 ? 2 : 4; }
 
-// True when, for every replica, segment s+1 starts right after segment s in
-// memory (for one pointer kind).
+// True when, for every replica, each non-empty segment starts right where
+// the previous non-empty one ends (for one pointer kind).
 bool back_to_back(void* const* p, int32_t n, int32_t S, const int64_t* numel, int esize) {
-  for (int32_t r = 0; r < n; ++r)
-    for (int32_t s = 0; s + 1 < S; ++s) {
+  for (int32_t r = 0; r < n; ++r) {
+    const char* end = nullptr;
+    for (int32_t s = 0; s < S; ++s) {
+      if (numel[s] == 0) continue;
       const char* a = static_cast<const char*>(p[(size_t)r * S + s]);
-      const char* b = static_cast<const char*>(p[(size_t)r * S + s + 1]);
-      if (numel[s] == 0 || numel[s + 1] == 0) return false;
-      if (a + numel[s] * esize != b) return false;
+      if (end && a != end) return false;
+      end = a + numel[s] * esize;
     }
+  }
   return true;
 }
 
-int32_t check_ptrs(void* const* p, const char* what, int32_t n, int32_t S, const int64_t* numel) {
+int32_t check_nonnull(void* const* p, const char* what, int32_t n, int32_t S,
+                      const int64_t* numel) {
+  for (int32_t r = 0; r < n; ++r)
+    for (int32_t s = 0; s < S; ++s)
+      if (numel[s] != 0 && !p[(size_t)r * S + s])
+        return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] is NULL", what, r, s);
+  return RIP_OK;
+}
+
+// Every address the kernel uses as a base must be 16-byte aligned: each
+// non-empty segment, or only the first one when the segments are coalesced.
+int32_t check_align(void* const* p, const char* what, int32_t n, int32_t S, const int64_t* numel,
+                    bool flat) {
   for (int32_t r = 0; r < n; ++r)
     for (int32_t s = 0; s < S; ++s) {
-      const void* q = p[(size_t)r * S + s];
       if (numel[s] == 0) continue;
-      if (!q) return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] is NULL", what, r, s);
+      const void* q = p[(size_t)r * S + s];
       if (reinterpret_cast<uintptr_t>(q) % 16 != 0)
         return rip::fail(RIP_E_ALIGN, "%s[%d*S+%d] = %p is not 16-byte aligned", what, r, s, q);
+      if (flat) break;
     }
   return RIP_OK;
 }
@@ -104,20 +118,25 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   for (int32_t s = 0; s < n_segments; ++s)
     if (seg_numel[s] < 0) return rip::fail(RIP_E_INVAL, "seg_numel[%d] < 0", s);
   int32_t rc;
-  if ((rc = check_ptrs(param, "param", n_replicas, n_segments, seg_numel)) != RIP_OK) return rc;
-  if (grad && (rc = check_ptrs(grad, "grad", n_replicas, n_segments, seg_numel)) != RIP_OK)
+  if ((rc = check_nonnull(param, "param", n_replicas, n_segments, seg_numel)) != RIP_OK) return rc;
+  if (grad && (rc = check_nonnull(grad, "grad", n_replicas, n_segments, seg_numel)) != RIP_OK)
     return rc;
-  if (mom && (rc = check_ptrs(mom, "mom", n_replicas, n_segments, seg_numel)) != RIP_OK)
+  if (mom && (rc = check_nonnull(mom, "mom", n_replicas, n_segments, seg_numel)) != RIP_OK)
     return rc;
 
   // Collapse back-to-back segments into one flat range per replica.
   const int esize = elem_size(dtype);
   int64_t total = 0;
   for (int32_t s = 0; s < n_segments; ++s) total += seg_numel[s];
-  const bool flat = n_segments == 1 ||
-                    (back_to_back(param, n_replicas, n_segments, seg_numel, esize) &&
-                     (!grad || back_to_back(grad, n_replicas, n_segments, seg_numel, esize)) &&
-                     (!mom || back_to_back(mom, n_replicas, n_segments, seg_numel, esize)));
+  const bool flat = back_to_back(param, n_replicas, n_segments, seg_numel, esize) &&
+                    (!grad || back_to_back(grad, n_replicas, n_segments, seg_numel, esize)) &&
+                    (!mom || back_to_back(mom, n_replicas, n_segments, seg_numel, esize));
+  if ((rc = check_align(param, "param", n_replicas, n_segments, seg_numel, flat)) != RIP_OK)
+    return rc;
+  if (grad && (rc = check_align(grad, "grad", n_replicas, n_segments, seg_numel, flat)) != RIP_OK)
+    return rc;
+  if (mom && (rc = check_align(mom, "mom", n_replicas, n_segments, seg_numel, flat)) != RIP_OK)
+    return rc;
   const int32_t S = flat ? 1 : n_segments;
   const int32_t N = n_replicas;
   std::vector<uint64_t> ptab((size_t)3 * S * N, 0);
@@ -127,7 +146,12 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
     numel[s] = flat ? total : seg_numel[s];
     tile0[s] = s == 0 ? 0 : tile0[s - 1] + (numel[s - 1] + tile_elems - 1) / tile_elems;
     for (int32_t r = 0; r < N; ++r) {
-      const size_t src = (size_t)r * n_segments + s;
+      size_t src = (size_t)r * n_segments + s;
+      if (flat) {  // the flat range starts at the first non-empty segment
+        int32_t s0 = 0;
+        while (s0 + 1 < n_segments && seg_numel[s0] == 0) ++s0;
+        src = (size_t)r * n_segments + s0;
+      }
       const size_t dst = (size_t)s * N + r;
       ptab[dst] = reinterpret_cast<uint64_t>(param[src]);
       ptab[(size_t)S * N + dst] = grad ? reinterpret_cast<uint64_t>(grad[src]) : 0;

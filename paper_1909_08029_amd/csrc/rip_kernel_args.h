@@ -9,8 +9,14 @@
 
 namespace rip {
 
-constexpr int kBlock = 256;  // threads per workgroup (4 wave64)
-constexpr int kSlots = 4;    // 16-byte slots per thread per tile
+#ifndef RIP_BLOCK
+#define RIP_BLOCK 256
+#endif
+#ifndef RIP_SLOTS
+#define RIP_SLOTS 4
+#endif
+constexpr int kBlock = RIP_BLOCK;  // threads per workgroup (wave64)
+constexpr int kSlots = RIP_SLOTS;  // 16-byte slots per thread per tile
 constexpr int kMaxK = 8;     // largest group size with a specialized path
 
 // Passed by value as the kernel argument (about 1.1 KiB), so each launch

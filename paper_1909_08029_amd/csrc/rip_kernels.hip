@@ -41,11 +41,33 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // address space so the compiler emits global_* (not flat_*) instructions.
 #define RIP_GLOBAL __attribute__((address_space(1)))
 
+// Streaming hints: every byte is touched once per step.
+#ifndef RIP_NT_LOAD
+#define RIP_NT_LOAD 1
+#endif
+#ifndef RIP_NT_STORE
+#define RIP_NT_STORE 1
+#endif
+#ifndef RIP_UNIT_MAJOR
+#define RIP_UNIT_MAJOR 1
+#endif
+#ifndef RIP_U_SCALE
+#define RIP_U_SCALE 2
+#endif
+
 __device__ __forceinline__ u32x4 ld16(const char* p) {
+#if RIP_NT_LOAD
   return __builtin_nontemporal_load((const RIP_GLOBAL u32x4*)p);
+#else
+  return *(const RIP_GLOBAL u32x4*)p;
+#endif
 }
 __device__ __forceinline__ void st16(char* p, u32x4 v) {
+#if RIP_NT_STORE
   __builtin_nontemporal_store(v, (RIP_GLOBAL u32x4*)p);
+#else
+  *(RIP_GLOBAL u32x4*)p = v;
+#endif
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
@@ -241,7 +263,8 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
 
 template <int K, bool BF16, bool MOM>
 __device__ __forceinline__ void full_tile(const StepArgs& a, int base, int seg, int64_t e_tile) {
-  constexpr int U = (K <= 2) ? 4 : (K <= 4 ? 2 : 1);
+  constexpr int U0 = ((K <= 2) ? 4 : (K <= 4 ? 2 : 1)) * RIP_U_SCALE;
+  constexpr int U = U0 > kSlots ? kSlots : U0;
   constexpr int N = Vec<BF16>::N;
   constexpr int esize = BF16 ? 2 : 4;
   Members m;
@@ -261,8 +284,14 @@ __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
   constexpr int64_t tile_elems = (int64_t)kBlock * kSlots * Vec<BF16>::N;
   const uint32_t tiles = (uint32_t)a.tiles;
   for (uint32_t w = blockIdx.x; w < (uint32_t)a.work; w += gridDim.x) {
+#if RIP_UNIT_MAJOR
     const int unit = (int)(w / tiles);
     const int64_t tile = (int64_t)(w - (uint32_t)unit * tiles);
+#else
+    const uint32_t nu = (uint32_t)a.n_units;
+    const int64_t tile = (int64_t)(w / nu);
+    const int unit = (int)(w - (uint32_t)tile * nu);
+#endif
     // segment holding this tile: the last s with seg_tile0[s] <= tile
     int lo = 0, hi = a.n_seg - 1;
     while (lo < hi) {
@@ -296,15 +325,13 @@ __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
 
 hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, int blocks,
                              hipStream_t stream) {
-  const dim3 grid(blocks), block(kBlock);
-  if (bf16) {
-    if (mom) hipLaunchKernelGGL((fused_step_kernel<true, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((fused_step_kernel<true, false>), grid, block, 0, stream, a);
-  } else {
-    if (mom) hipLaunchKernelGGL((fused_step_kernel<false, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((fused_step_kernel<false, false>), grid, block, 0, stream, a);
-  }
-  return hipGetLastError();
+  const void* fn = bf16 ? (mom ? reinterpret_cast<const void*>(&fused_step_kernel<true, true>)
+                               : reinterpret_cast<const void*>(&fused_step_kernel<true, false>))
+                        : (mom ? reinterpret_cast<const void*>(&fused_step_kernel<false, true>)
+                               : reinterpret_cast<const void*>(&fused_step_kernel<false, false>));
+  void* args[] = {const_cast<StepArgs*>(&a)};
+  // hipLaunchKernel reports this launch's own status (not an earlier sticky error).
+  return hipLaunchKernel(fn, dim3(blocks), dim3(kBlock), args, 0, stream);
 }
 
 }  // namespace rip

@@ -134,6 +134,7 @@ _lib = None
 def gpu_lib():
     global _lib
     if _lib is None:
+        import torch  # noqa: F401  -- bind to torch's HIP runtime (see the binding)
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
         lib = ctypes.CDLL(LIB_PATH)

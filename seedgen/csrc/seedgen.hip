@@ -54,11 +54,8 @@ extern "C" int32_t seedgen_fill_normal(void* dst, int32_t dtype, uint64_t key, i
   int64_t blocks = (count + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dtype == 0)
-    hipLaunchKernelGGL(fill_f32, dim3((unsigned)blocks), dim3(256), 0, s,
-                       static_cast<float*>(dst), key, start, count, scale);
-  else
-    hipLaunchKernelGGL(fill_bf16, dim3((unsigned)blocks), dim3(256), 0, s,
-                       static_cast<uint16_t*>(dst), key, start, count, scale);
-  return hipGetLastError() == hipSuccess ? 0 : -5;
+  const void* fn = dtype == 0 ? reinterpret_cast<const void*>(&fill_f32)
+                              : reinterpret_cast<const void*>(&fill_bf16);
+  void* args[] = {&dst, &key, &start, &count, &scale};
+  return hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(256), args, 0, s) == hipSuccess ? 0 : -5;
 }
