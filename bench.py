@@ -106,6 +106,8 @@ def main():
     ap.add_argument("--grad-ring", type=int, default=None)
     ap.add_argument("--max-blocks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device copy of known size (to scale HBM counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -124,6 +126,17 @@ def main():
         err("no GPU visible")
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = 1 << 30                                    # 4 GiB of fp32 each way
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read_per_launch": 4 * n,
+                          "bytes_written_per_launch": 4 * n, "launches": 5}), flush=True)
+        return
     w = wl.CONFIGS[args.config]
     if args.grad_ring:
         w = wl.scaled(w, w.seg_numel, grad_ring=args.grad_ring)

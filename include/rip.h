@@ -229,8 +229,12 @@ int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offsets,
                     const int32_t* members, int32_t n_groups, const int32_t* active,
                     int32_t n_active, const rip_sgd* sgd, void* stream);
 
-/* Launch tuning: cap on workgroups per launch (0 = library default). */
+/* Launch tuning (process-wide).  rip_set_max_blocks caps the workgroups of
+ * one launch (0 = one workgroup per tile); rip_set_blocks_per_cu caps how
+ * many of the kernel's workgroups share a compute unit (0 = the library's
+ * measured default for the storage type and optimizer). */
 int32_t rip_set_max_blocks(int32_t max_blocks);
+int32_t rip_set_blocks_per_cu(int32_t blocks_per_cu);
 
 #ifdef __cplusplus
 }

@@ -90,6 +90,7 @@ def _load():
         "rip_preduce": (ctypes.c_int32, [vp, _i32p, _i32p, ctypes.c_int32, _i32p,
                                          ctypes.c_int32, ctypes.POINTER(Sgd), vp]),
         "rip_set_max_blocks": (ctypes.c_int32, [ctypes.c_int32]),
+        "rip_set_blocks_per_cu": (ctypes.c_int32, [ctypes.c_int32]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -275,6 +276,10 @@ def rip_preduce(rep: Replicas, groups: Sequence[Sequence[int]], active: Sequence
 
 def rip_set_max_blocks(n: int) -> None:
     _check(lib.rip_set_max_blocks(n))
+
+
+def rip_set_blocks_per_cu(n: int) -> None:
+    _check(lib.rip_set_blocks_per_cu(n))
 
 
 def abi_version() -> int:

@@ -1,7 +1,7 @@
 """Build librip.so (the P-Reduce library) and libseedgen.so (input generator)
 in-tree with hipcc for gfx950.
 
-    python -m paper_1909_08029_amd.build        # or __graft_entry__.build()
+    python paper_1909_08029_amd/build.py        # or __graft_entry__.build()
 
 Always recompiles.  Flags: -O3, fp contraction off (the kernels' arithmetic
 order is part of their contract), packed-fp32 instructions disabled.

@@ -20,6 +20,7 @@ namespace rip {
 namespace {
 thread_local std::string g_last_error;
 std::atomic<int> g_max_blocks{0};
+std::atomic<int> g_blocks_per_cu{0};
 constexpr int kDefaultMaxBlocks = 1 << 20;
 }  // namespace
 
@@ -39,9 +40,10 @@ void clear_error() { g_last_error.clear(); }
 
 struct rip_replicas {
   int32_t n = 0, n_seg = 0, dtype = 0, device = 0;
+  int32_t lds_per_cu = 0;  // bytes of LDS per compute unit on `device`
   bool has_grad = false, has_mom = false;
-  int64_t tiles = 0;
-  void* dmem = nullptr;  // ptab [3][S][N] u64 | seg_numel [S] i64 | seg_tile0 [S+1] i64
+  int64_t tiles[rip::kTileOptions] = {};  // tiles per unit, by slot option
+  void* dmem = nullptr;  // ptab [3][S][N] u64 | seg_numel [S] i64 | seg_tile0 [4][S+1] i64
   const uint64_t* d_ptab = nullptr;
   const int64_t* d_numel = nullptr;
   const int64_t* d_tile0 = nullptr;
@@ -50,6 +52,12 @@ struct rip_replicas {
 extern "C" const char* rip_last_error(void) { return rip::g_last_error.c_str(); }
 extern "C" int32_t rip_abi_version(void) { return RIP_ABI_VERSION; }
 
+extern "C" int32_t rip_set_blocks_per_cu(int32_t blocks_per_cu) {
+  if (blocks_per_cu < 0) return rip::fail(RIP_E_INVAL, "blocks_per_cu must be >= 0");
+  rip::g_blocks_per_cu.store(blocks_per_cu);
+  return RIP_OK;
+}
+
 extern "C" int32_t rip_set_max_blocks(int32_t max_blocks) {
   if (max_blocks < 0) return rip::fail(RIP_E_INVAL, "max_blocks must be >= 0");
   rip::g_max_blocks.store(max_blocks);
@@ -57,6 +65,13 @@ extern "C" int32_t rip_set_max_blocks(int32_t max_blocks) {
 }
 
 namespace {
+
+// Waves per CU at which the fused kernel sustained the most HBM bandwidth on
+// MI355X (measured over workgroup caps of 4-12 waves per CU): more resident
+// waves add outstanding requests without adding bandwidth.  bf16 storage
+// does more ALU work per byte and peaks with fewer waves; momentum moves five
+// streams per member and peaks slightly below plain SGD.
+int target_waves_per_cu(bool bf16, bool mom) { return bf16 ? 8 : (mom ? 9 : 10); }
 
 int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
 int elem_size(int32_t dtype) { return dtype == RIP_BF16 ? 2 : 4; }
@@ -140,11 +155,9 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   const int32_t S = flat ? 1 : n_segments;
   const int32_t N = n_replicas;
   std::vector<uint64_t> ptab((size_t)3 * S * N, 0);
-  std::vector<int64_t> numel(S), tile0(S + 1);
-  const int64_t tile_elems = (int64_t)rip::kBlock * rip::kSlots * elems_per_16b(dtype);
+  std::vector<int64_t> numel(S), tile0((size_t)rip::kTileOptions * (S + 1));
   for (int32_t s = 0; s < S; ++s) {
     numel[s] = flat ? total : seg_numel[s];
-    tile0[s] = s == 0 ? 0 : tile0[s - 1] + (numel[s - 1] + tile_elems - 1) / tile_elems;
     for (int32_t r = 0; r < N; ++r) {
       size_t src = (size_t)r * n_segments + s;
       if (flat) {  // the flat range starts at the first non-empty segment
@@ -158,7 +171,13 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
       ptab[(size_t)2 * S * N + dst] = mom ? reinterpret_cast<uint64_t>(mom[src]) : 0;
     }
   }
-  tile0[S] = tile0[S - 1] + (numel[S - 1] + tile_elems - 1) / tile_elems;
+  // First tile of every segment, for each tile size (1, 2, 4, 8 slots).
+  for (int o = 0; o < rip::kTileOptions; ++o) {
+    const int64_t tile_elems = ((int64_t)rip::kBlock * elems_per_16b(dtype)) << o;
+    int64_t* t0 = tile0.data() + (size_t)o * (S + 1);
+    t0[0] = 0;
+    for (int32_t s = 0; s < S; ++s) t0[s + 1] = t0[s] + (numel[s] + tile_elems - 1) / tile_elems;
+  }
 
   rip_replicas* h = new (std::nothrow) rip_replicas();
   if (!h) return rip::fail(RIP_E_NOMEM, "out of host memory");
@@ -167,10 +186,13 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   h->dtype = dtype;
   h->has_grad = grad != nullptr;
   h->has_mom = mom != nullptr;
-  h->tiles = tile0[S];
+  for (int o = 0; o < rip::kTileOptions; ++o) h->tiles[o] = tile0[(size_t)o * (S + 1) + S];
   hipError_t e = hipGetDevice(&h->device);
+  if (e == hipSuccess)
+    e = hipDeviceGetAttribute(&h->lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                              h->device);
   const size_t bytes_ptab = ptab.size() * sizeof(uint64_t);
-  const size_t bytes = bytes_ptab + (size_t)S * 8 + (size_t)(S + 1) * 8;
+  const size_t bytes = bytes_ptab + (size_t)S * 8 + tile0.size() * 8;
   if (e == hipSuccess) e = hipMalloc(&h->dmem, bytes);
   if (e != hipSuccess) {
     delete h;
@@ -181,7 +203,7 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   std::vector<char> staging(bytes);
   std::memcpy(staging.data(), ptab.data(), bytes_ptab);
   std::memcpy(staging.data() + bytes_ptab, numel.data(), (size_t)S * 8);
-  std::memcpy(staging.data() + bytes_ptab + (size_t)S * 8, tile0.data(), (size_t)(S + 1) * 8);
+  std::memcpy(staging.data() + bytes_ptab + (size_t)S * 8, tile0.data(), tile0.size() * 8);
   e = hipMemcpy(d, staging.data(), bytes, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(h->dmem);
@@ -207,7 +229,7 @@ namespace {
 // order given, then active workers outside every group, ascending).
 int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const int32_t* members,
                    int32_t n_groups, const int32_t* active, int32_t n_active, const rip_sgd* sgd,
-                   rip::StepArgs& a) {
+                   rip::StepArgs& a, bool& mom) {
   const int32_t N = r->n;
   if (n_groups < 0 || n_active < 0) return rip::fail(RIP_E_INVAL, "negative count");
   if (n_groups > 0 && (!group_offsets || !members))
@@ -262,16 +284,22 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
   a.ptab = r->d_ptab;
   a.seg_numel = r->d_numel;
   a.seg_tile0 = r->d_tile0;
-  a.tiles = r->tiles;
-  a.work = (int64_t)units * r->tiles;
-  if (a.work >= (int64_t)1 << 31)
-    return rip::fail(RIP_E_UNSUPPORTED, "%lld work items exceed 2^31 (segments too large)",
-                     (long long)a.work);
   a.n_seg = r->n_seg;
   a.n_rep = N;
   a.n_units = units;
   a.lr = sgd ? sgd->lr : 0.0f;
   a.mu = sgd ? sgd->momentum : 0.0f;
+  mom = sgd && sgd->momentum != 0.0f && n_active > 0;
+  int64_t work = 0;
+  a.unit_work0[0] = 0;
+  for (int32_t u = 0; u < units; ++u) {
+    const int k = a.unit_off[u + 1] - a.unit_off[u];
+    work += r->tiles[rip::slot_log2(k, mom)];
+    if (work >= (int64_t)1 << 31)
+      return rip::fail(RIP_E_UNSUPPORTED, "more than 2^31 tiles in one step (replicas too large)");
+    a.unit_work0[u + 1] = (uint32_t)work;
+  }
+  a.work = (uint32_t)work;
   return RIP_OK;
 }
 
@@ -283,7 +311,8 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   rip::clear_error();
   if (!r) return rip::fail(RIP_E_INVAL, "rip_preduce: replicas handle is NULL");
   rip::StepArgs a;
-  int32_t rc = build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a);
+  bool mom = false;
+  int32_t rc = build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a, mom);
   if (rc != RIP_OK) return rc;
   if (a.work == 0) return RIP_OK;
   int dev = -1;
@@ -294,8 +323,11 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
                      r->device);
   const int cap = rip::g_max_blocks.load() > 0 ? rip::g_max_blocks.load() : rip::kDefaultMaxBlocks;
   const int blocks = (int)(a.work < cap ? a.work : cap);
-  const bool mom = a.mu != 0.0f && n_active > 0;
-  e = rip::launch_fused_step(a, r->dtype == RIP_BF16, mom, blocks,
+  int bpc = rip::g_blocks_per_cu.load();
+  if (bpc == 0) bpc = target_waves_per_cu(r->dtype == RIP_BF16, mom) * 64 / rip::kBlock;
+  size_t lds = 0;
+  if (bpc > 0 && r->lds_per_cu > 0) lds = (size_t)(r->lds_per_cu / bpc) & ~(size_t)255;
+  e = rip::launch_fused_step(a, r->dtype == RIP_BF16, mom, blocks, lds,
                              static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return rip::fail(RIP_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   return RIP_OK;

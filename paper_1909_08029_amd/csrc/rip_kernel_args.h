@@ -10,31 +10,46 @@
 namespace rip {
 
 #ifndef RIP_BLOCK
-#define RIP_BLOCK 256
+#define RIP_BLOCK 64
 #endif
-#ifndef RIP_SLOTS
-#define RIP_SLOTS 4
+#ifndef RIP_LOADS_IN_FLIGHT
+#define RIP_LOADS_IN_FLIGHT 24
 #endif
-constexpr int kBlock = RIP_BLOCK;  // threads per workgroup (wave64)
-constexpr int kSlots = RIP_SLOTS;  // 16-byte slots per thread per tile
-constexpr int kMaxK = 8;     // largest group size with a specialized path
+constexpr int kBlock = RIP_BLOCK;  // threads per workgroup: one wave64
+constexpr int kMaxK = 8;           // largest group size with a specialized path
+constexpr int kTileOptions = 4;    // tiles of 1, 2, 4 or 8 slots per thread
 
-// Passed by value as the kernel argument (about 1.1 KiB), so each launch
+// A tile of a unit is kBlock threads x 2^slot_log2 slots x 16 bytes of each
+// member stream.  The slot count keeps about RIP_LOADS_IN_FLIGHT 16-byte
+// loads outstanding per thread (k members x w, g and, with momentum, v), so
+// small groups and lone updates still have enough bytes in flight while a
+// workgroup moves a similar number of bytes whatever the group size.  Groups
+// above kMaxK take the element-wise path with one slot.
+constexpr int slot_log2(int k, bool mom) {
+  if (k > kMaxK) return 0;
+  const int s = RIP_LOADS_IN_FLIGHT / (k * (mom ? 3 : 2));
+  int l = 0;
+  while (l < kTileOptions - 1 && (2 << l) <= s) ++l;
+  return l;
+}
+
+// Passed by value as the kernel argument (about 2.2 KiB), so each launch
 // carries its own schedule and no device staging buffer is needed.
 struct StepArgs {
   const uint64_t* ptab;       // device [3][S][N]: param, grad, mom pointers
   const int64_t* seg_numel;   // device [S]
-  const int64_t* seg_tile0;   // device [S + 1]: first tile of each segment
-  int64_t tiles;              // tiles per unit (seg_tile0[S])
-  int64_t work;               // units * tiles
-  int32_t n_seg, n_rep, n_units, reserved;
+  const int64_t* seg_tile0;   // device [kTileOptions][S + 1]: first tile of each
+                              // segment, for tiles of 1, 2, 4, 8 slots
+  int32_t n_seg, n_rep, n_units;
+  uint32_t work;              // work items (tiles) of all units
   float lr, mu;
-  uint16_t unit_off[RIP_MAX_REPLICAS + 1];  // unit u = member[unit_off[u] .. unit_off[u+1])
-  uint16_t member[RIP_MAX_REPLICAS];        // replica ids, ascending within a unit
+  uint32_t unit_work0[RIP_MAX_REPLICAS + 1];  // first work item of each unit
+  uint16_t unit_off[RIP_MAX_REPLICAS + 1];    // unit u = member[unit_off[u] .. unit_off[u+1])
+  uint16_t member[RIP_MAX_REPLICAS];          // replica ids, ascending within a unit
   uint32_t active_bits[RIP_MAX_REPLICAS / 32];  // replicas doing their local update
 };
 
 hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, int blocks,
-                             hipStream_t stream);
+                             size_t lds_bytes, hipStream_t stream);
 
 }  // namespace rip

@@ -6,13 +6,18 @@
 // updates without synchronizing.  Disjoint groups run concurrently (Sec. 3.2).
 //
 // Work decomposition.  Every unit touches the same element range of its
-// members' buffers, so the launch is a grid of (unit, tile) work items; a
-// tile is 256 threads x 4 slots x 16 bytes of each member stream.  A
-// workgroup handles one unit at a time, so the unit's size k, its member ids
-// and their active flags are wave-uniform: they sit in scalar registers and
-// every branch on them is a scalar branch.  Each thread keeps the loads of
-// all k members (and their gradients / momenta) of one or more 16-byte slots
-// in flight before any arithmetic, then writes the mean back to every member.
+// members' buffers, so the launch is a list of (unit, tile) work items, one
+// per single-wave workgroup, unit after unit.  A tile is 64 lanes x 1-8
+// slots x 16 bytes of each member stream; the slot count shrinks as the
+// unit's number of streams grows (see slot_log2), so every wave keeps about
+// 24 16-byte loads in flight per lane whatever the group size.  The host caps
+// residency at 8-10 waves per CU (an LDS reservation): HBM3E delivered its
+// best rate at that depth of outstanding requests, not at full occupancy.  A workgroup
+// handles one unit, so the unit's size k, its member ids and their active
+// flags are wave-uniform: they sit in scalar registers and every branch on
+// them is a scalar branch.  Each thread issues the loads of all members
+// (and their gradients / momenta) for all its slots before any arithmetic,
+// then writes the mean back to every member.
 //
 // The operation is a stream over HBM with no data reuse and about one flop
 // per 4 bytes, so there is no LDS tiling and no matrix-core work: the design
@@ -47,12 +52,6 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 #endif
 #ifndef RIP_NT_STORE
 #define RIP_NT_STORE 1
-#endif
-#ifndef RIP_UNIT_MAJOR
-#define RIP_UNIT_MAJOR 1
-#endif
-#ifndef RIP_U_SCALE
-#define RIP_U_SCALE 2
 #endif
 
 __device__ __forceinline__ u32x4 ld16(const char* p) {
@@ -263,46 +262,42 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
 
 template <int K, bool BF16, bool MOM>
 __device__ __forceinline__ void full_tile(const StepArgs& a, int base, int seg, int64_t e_tile) {
-  constexpr int U0 = ((K <= 2) ? 4 : (K <= 4 ? 2 : 1)) * RIP_U_SCALE;
-  constexpr int U = U0 > kSlots ? kSlots : U0;
+  constexpr int SL = 1 << slot_log2(K, MOM);
   constexpr int N = Vec<BF16>::N;
   constexpr int esize = BF16 ? 2 : 4;
   Members m;
   load_members<K>(a, base, seg, m);
+  int64_t off[SL];
 #pragma unroll
-  for (int s0 = 0; s0 < kSlots; s0 += U) {
-    int64_t off[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      off[u] = (e_tile + (int64_t)((s0 + u) * kBlock + (int)threadIdx.x) * N) * esize;
-    tile_slots<K, U, BF16, MOM>(m, off, a.lr, a.mu);
+  for (int u = 0; u < SL; ++u)
+    off[u] = (e_tile + (int64_t)(u * kBlock + (int)threadIdx.x) * N) * esize;
+  tile_slots<K, SL, BF16, MOM>(m, off, a.lr, a.mu);
+}
+
+// Last index i in [0, n) with v[i] <= x (v ascending, v[0] <= x).
+template <typename T, typename X>
+__device__ __forceinline__ int last_le(const T* v, int n, X x) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((X)v[mid] <= x) lo = mid; else hi = mid - 1;
   }
+  return lo;
 }
 
 template <bool BF16, bool MOM>
 __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
-  constexpr int64_t tile_elems = (int64_t)kBlock * kSlots * Vec<BF16>::N;
-  const uint32_t tiles = (uint32_t)a.tiles;
-  for (uint32_t w = blockIdx.x; w < (uint32_t)a.work; w += gridDim.x) {
-#if RIP_UNIT_MAJOR
-    const int unit = (int)(w / tiles);
-    const int64_t tile = (int64_t)(w - (uint32_t)unit * tiles);
-#else
-    const uint32_t nu = (uint32_t)a.n_units;
-    const int64_t tile = (int64_t)(w / nu);
-    const int unit = (int)(w - (uint32_t)tile * nu);
-#endif
-    // segment holding this tile: the last s with seg_tile0[s] <= tile
-    int lo = 0, hi = a.n_seg - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.seg_tile0[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    const int seg = lo;
-    const int64_t e_tile = (tile - a.seg_tile0[seg]) * tile_elems;
-    const int64_t numel = a.seg_numel[seg];
+  for (uint32_t w = blockIdx.x; w < a.work; w += gridDim.x) {
+    const int unit = last_le(a.unit_work0, a.n_units, w);
+    const int64_t tile = (int64_t)(w - a.unit_work0[unit]);
     const int base = a.unit_off[unit];
     const int k = a.unit_off[unit + 1] - base;
+    const int o = slot_log2(k, MOM);
+    const int64_t* tile0 = a.seg_tile0 + o * (a.n_seg + 1);
+    const int seg = last_le(tile0, a.n_seg, tile);
+    const int64_t tile_elems = ((int64_t)kBlock * Vec<BF16>::N) << o;
+    const int64_t e_tile = (tile - tile0[seg]) * tile_elems;
+    const int64_t numel = a.seg_numel[seg];
     if (e_tile + tile_elems <= numel) {
       switch (k) {
         case 1: full_tile<1, BF16, MOM>(a, base, seg, e_tile); continue;
@@ -324,14 +319,16 @@ __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
 }  // namespace
 
 hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, int blocks,
-                             hipStream_t stream) {
+                             size_t lds_bytes, hipStream_t stream) {
   const void* fn = bf16 ? (mom ? reinterpret_cast<const void*>(&fused_step_kernel<true, true>)
                                : reinterpret_cast<const void*>(&fused_step_kernel<true, false>))
                         : (mom ? reinterpret_cast<const void*>(&fused_step_kernel<false, true>)
                                : reinterpret_cast<const void*>(&fused_step_kernel<false, false>));
   void* args[] = {const_cast<StepArgs*>(&a)};
   // hipLaunchKernel reports this launch's own status (not an earlier sticky error).
-  return hipLaunchKernel(fn, dim3(blocks), dim3(kBlock), args, 0, stream);
+  // lds_bytes is a reservation only (the kernel uses no LDS): it caps how
+  // many workgroups share a CU.
+  return hipLaunchKernel(fn, dim3(blocks), dim3(kBlock), args, lds_bytes, stream);
 }
 
 }  // namespace rip

@@ -119,43 +119,53 @@ class DeviceState:
 
     layout "flat": one buffer per replica and kind, segments are views into
     it back to back (the zero-copy form of flattening the model, Sec. 5.1).
-    layout "separate": every segment is its own allocation."""
+    layout "separate": every segment is its own allocation.
+    layout "arena": one allocation per kind holding every replica's flat
+    buffer at a pitch of (P * element size rounded up to 256 bytes) + pad."""
 
-    def __init__(self, w: Workload, layout: str = "flat", device: str = "cuda"):
+    def __init__(self, w: Workload, layout: str = "flat", device: str = "cuda", pad: int = 0):
         import torch
         self.w, self.layout = w, layout
         tdt = torch.bfloat16 if w.dtype == DTYPE_BF16 else torch.float32
         P = w.numel
         offs = np.concatenate([[0], np.cumsum(w.seg_numel)]).astype(np.int64)
         self.seg_off = [int(o) for o in offs]
+        nseg = len(w.seg_numel)
+        pitch = ((P * w.esize + 255) // 256) * 256 + pad
+        if layout == "arena" and pitch % 16:
+            raise ValueError("arena pad must keep 16-byte alignment")
 
-        def alloc():
+        def views(flat):
+            return [flat[self.seg_off[s]:self.seg_off[s + 1]] for s in range(nseg)]
+
+        def alloc_kind():
+            """Returns per-replica (flat tensor or None, segment views)."""
+            if layout == "arena":
+                arena = torch.empty(w.n * pitch, dtype=torch.uint8, device=device)
+                out = []
+                for r in range(w.n):
+                    flat = arena[r * pitch:r * pitch + P * w.esize].view(tdt)
+                    out.append((flat, views(flat)))
+                return out
             if layout == "flat":
-                flat = torch.empty(P, dtype=tdt, device=device)
-                return flat, [flat[self.seg_off[s]:self.seg_off[s + 1]]
-                              for s in range(len(w.seg_numel))]
-            segs = [torch.empty(m, dtype=tdt, device=device) for m in w.seg_numel]
-            return None, segs
+                out = []
+                for r in range(w.n):
+                    flat = torch.empty(P, dtype=tdt, device=device)
+                    out.append((flat, views(flat)))
+                return out
+            return [(None, [torch.empty(m, dtype=tdt, device=device) for m in w.seg_numel])
+                    for r in range(w.n)]
 
-        self.param_flat, self.param = [], []
-        for r in range(w.n):
-            f, segs = alloc()
-            self.param_flat.append(f)
-            self.param.append(segs)
-        self.grad_sets = []
-        for slot in range(w.grad_ring):
-            gs = []
-            for r in range(w.n):
-                gs.append(alloc()[1])
-            self.grad_sets.append(gs)
+        kind = alloc_kind()
+        self.param_flat = [f for f, _ in kind]
+        self.param = [segs for _, segs in kind]
+        self.grad_sets = [[segs for _, segs in alloc_kind()] for _ in range(w.grad_ring)]
         self.mom = None
         if w.momentum:
-            self.mom = []
-            for r in range(w.n):
-                segs = alloc()[1]
+            self.mom = [segs for _, segs in alloc_kind()]
+            for segs in self.mom:
                 for t in segs:
                     t.zero_()
-                self.mom.append(segs)
 
     def fill(self):
         """Parameters and every gradient set from the seeded generator."""
