@@ -72,11 +72,19 @@ __device__ __forceinline__ void st16(char* p, u32x4 v) {
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xFFFF0000u); }
 
-// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t bf16_round(float f) {
-  const uint32_t b = __float_as_uint(f);
-  const uint32_t r = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
-  return ((b & 0x7FFFFFFFu) > 0x7F800000u) ? ((b >> 16) | 0x40u) : r;
+// fp32 -> bf16, round to nearest even, NaN kept quiet: gfx950's
+// v_cvt_pk_bf16_f32 (what clang emits for a conversion to __bf16), two values
+// per instruction.  Its results equal the round-to-nearest-even definition
+// for all 2^32 fp32 inputs (checked exhaustively on the GPU).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t bf16_pack2(float lo, float hi) {
+  const f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+}
+__device__ __forceinline__ uint16_t bf16_round(float f) {
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 template <bool BF16>
@@ -114,10 +122,10 @@ struct Vec<true> {
   }
   static __device__ __forceinline__ u32x4 pack(const float (&f)[N]) {
     u32x4 x;
-    x.x = bf16_round(f[0]) | (bf16_round(f[1]) << 16);
-    x.y = bf16_round(f[2]) | (bf16_round(f[3]) << 16);
-    x.z = bf16_round(f[4]) | (bf16_round(f[5]) << 16);
-    x.w = bf16_round(f[6]) | (bf16_round(f[7]) << 16);
+    x.x = bf16_pack2(f[0], f[1]);
+    x.y = bf16_pack2(f[2], f[3]);
+    x.z = bf16_pack2(f[4], f[5]);
+    x.w = bf16_pack2(f[6], f[7]);
     return x;
   }
 };
@@ -133,7 +141,7 @@ __device__ __forceinline__ float ld1(const char* base, int64_t e) {
 template <bool BF16>
 __device__ __forceinline__ void st1(char* base, int64_t e, float v) {
   if constexpr (BF16)
-    ((RIP_GLOBAL uint16_t*)base)[e] = (uint16_t)bf16_round(v);
+    ((RIP_GLOBAL uint16_t*)base)[e] = bf16_round(v);
   else
     ((RIP_GLOBAL float*)base)[e] = v;
 }
