@@ -85,7 +85,8 @@ def cpu_baseline(w, seconds: float = 12.0):
         active, groups = sch.step(steps, w.eligible(steps))
         g = grad(w.grad_slot(steps))
         t0 = time.perf_counter()
-        p, v = op.step(p, g, v, groups, active, w.lr, w.momentum or None, dt)
+        p, v = op.step(p, g, v, groups, active, w.lr, w.momentum or None, dt, True,
+                       w.weight_decay, w.nesterov)
         spent += time.perf_counter() - t0
         nbytes += sub.alg_bytes(active, groups)
         steps += 1
@@ -161,7 +162,8 @@ def main():
         h = handles[w.grad_slot(t)]
         if ev is not None:
             ev[0].record(stream)
-        rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, stream=stream)
+        rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, stream=stream,
+                        weight_decay=w.weight_decay, nesterov=w.nesterov)
         if ev is not None:
             ev[1].record(stream)
         t += 1

@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define RIP_ABI_VERSION 1
+#define RIP_ABI_VERSION 2
 
 /* status codes */
 enum {
@@ -196,8 +196,10 @@ void rip_replicas_destroy(rip_replicas* r); /* NULL is a no-op */
  * Local update and P-Reduce (Steps 2 and 4 of Fig. 4; F^G of Sec. 3.2)
  *
  * Arithmetic (fp32, this exact order; no fused multiply-add):
- *   active worker r:  u_r = w_r - lr*g_r, or with momentum
- *                     v_r = mu*v_r + g_r (stored), u_r = w_r - lr*v_r
+ *   active worker r:  g' = g_r + wd*w_r when weight_decay != 0, else g' = g_r;
+ *                     u_r = w_r - lr*g', or with momentum
+ *                     v_r = mu*v_r + g' (stored) and u_r = w_r - lr*v_r
+ *                     (Nesterov: u_r = w_r - lr*(g' + mu*v_r))
  *   other worker r:   u_r = w_r
  *   group m1 < ... < mk:  s = u_m1; s = s + u_mj (j = 2..k, ascending);
  *                     xbar = s * (float)(1.0/k); w_m = xbar for every member
@@ -206,15 +208,20 @@ void rip_replicas_destroy(rip_replicas* r); /* NULL is a no-op */
  * bf16 storage: values widen exactly to fp32 and are rounded to nearest-even
  * once, when stored.  Momentum buffers are never averaged (Step 4 averages
  * parameters only).  momentum == 0 is plain SGD and leaves mom untouched.
+ * The paper's ResNet-50 runs use momentum 0.9 and weight decay 1e-4
+ * (Sec. 6.1.2); its VGG-16 runs plain SGD.
  * ---------------------------------------------------------------------- */
 typedef struct rip_sgd {
-  float lr;        /* learning rate (eta in Fig. 4) */
-  float momentum;  /* mu; 0 = plain SGD.  Needs mom buffers when nonzero. */
+  float lr;            /* learning rate (eta in Fig. 4) */
+  float momentum;      /* mu; 0 = plain SGD.  Needs mom buffers when nonzero. */
+  float weight_decay;  /* wd, added to the gradient as wd*w; 0 = none */
+  int32_t nesterov;    /* nonzero: Nesterov momentum (needs momentum != 0) */
 } rip_sgd;
 
 /* Step 2 alone for the `n_active` workers listed in `active` (distinct ids).
  * Same as rip_preduce with no groups.
- * Errors: RIP_E_INVAL (null handle/sgd, ids, no grad or needed mom buffers). */
+ * Errors: RIP_E_INVAL (null handle/sgd, ids, no grad or needed mom buffers,
+ * Nesterov without momentum). */
 int32_t rip_local_step(const rip_replicas* r, const int32_t* active, int32_t n_active,
                        const rip_sgd* sgd, void* stream);
 

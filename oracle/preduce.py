@@ -6,8 +6,10 @@ algorithm using P-Reduce"):
   Step 2 (local update), for every worker i that computes this step:
       x_i <- x_i - eta * grad_i
     With the momentum optimizer the paper uses for ResNet-50 (Sec. 6.1.2,
-    momentum 0.9), the update is the usual heavy-ball form:
-      v_i <- mu * v_i + grad_i ;  x_i <- x_i - eta * v_i
+    momentum 0.9, weight decay 1e-4), the update is the usual heavy-ball form:
+      g <- grad_i + wd * x_i   (when weight decay is on)
+      v_i <- mu * v_i + g ;  x_i <- x_i - eta * v_i
+    or, with Nesterov momentum, x_i <- x_i - eta * (g + mu * v_i).
   Step 4 (P-Reduce of a group G, applied to every member):
       xbar_G = (1/|G|) * sum_{g in G} x_g ;  x_g <- xbar_G for g in G
     which is X <- X F^G with F^G_{ij} = 1/|G| for i, j in G and
@@ -19,9 +21,10 @@ bytes, Sec. 6.1.2); replicas are stored as fp32, or as bf16 with fp32
 arithmetic.  The oracle therefore computes in fp32, with one fixed order of
 operations so that a correct kernel can match it exactly:
 
-  * update:   u = fl(w - fl(eta*g)); momentum: v' = fl(fl(mu*v) + g),
-              u = fl(w - fl(eta*v'))  -- two roundings each, never a fused
-              multiply-add;
+  * update:   g' = fl(g + fl(wd*w)) if wd != 0; u = fl(w - fl(eta*g'));
+              momentum: v' = fl(fl(mu*v) + g'), u = fl(w - fl(eta*v')), or
+              Nesterov u = fl(w - fl(eta*fl(g' + fl(mu*v'))))  -- one rounding
+              per operation, never a fused multiply-add;
   * group sum: s = u_{m1}; s = fl(s + u_{mj}) for members in ascending order;
   * mean:     xbar = fl(s * fl32(1/|G|))  -- the literal "1/|G| times the
               sum"; fl32(1/k) is the fp32 rounding of the double 1/k;
@@ -91,13 +94,17 @@ def inv_k(k: int) -> np.float32:
 # Step 2: local update
 # ---------------------------------------------------------------------------
 def local_update(w: np.ndarray, g: np.ndarray, v: np.ndarray | None, lr: float,
-                 momentum: float | None):
+                 momentum: float | None, weight_decay: float = 0.0, nesterov: bool = False):
     """One worker's update in fp32.  Returns (u, v_new); v_new is None for SGD."""
     lr32 = np.float32(lr)
+    if weight_decay:
+        g = g + np.float32(weight_decay) * w
     if momentum is None:
         return w - lr32 * g, None
     mu32 = np.float32(momentum)
     v_new = mu32 * v + g
+    if nesterov:
+        return w - lr32 * (g + mu32 * v_new), v_new
     return w - lr32 * v_new, v_new
 
 
@@ -133,7 +140,8 @@ def _check_schedule(n: int, groups: Sequence[Sequence[int]], active: Iterable[in
 
 def step(param: np.ndarray, grad: np.ndarray | None, mom: np.ndarray | None,
          groups: Sequence[Sequence[int]], active: Iterable[int], lr: float = 0.0,
-         momentum: float | None = None, dtype: str = F32, fused: bool = True):
+         momentum: float | None = None, dtype: str = F32, fused: bool = True,
+         weight_decay: float = 0.0, nesterov: bool = False):
     """One step on all replicas.
 
     param, grad, mom: arrays of shape (N, P) holding the stored values
@@ -157,7 +165,7 @@ def step(param: np.ndarray, grad: np.ndarray | None, mom: np.ndarray | None,
         w = load(param[r], dtype)
         g = load(grad[r], dtype)
         v = None if momentum is None else load(mom[r], dtype)
-        u[r], v_new = local_update(w, g, v, lr, momentum)
+        u[r], v_new = local_update(w, g, v, lr, momentum, weight_decay, nesterov)
         if v_new is not None:
             new_mom[r] = store(v_new, dtype)
     if not fused:
@@ -185,10 +193,12 @@ def preduce(param: np.ndarray, groups: Sequence[Sequence[int]], dtype: str = F32
 
 
 def run(param0: np.ndarray, mom0: np.ndarray | None, grad_fn, schedule: Sequence,
-        lr: float, momentum: float | None, dtype: str = F32, fused: bool = True):
+        lr: float, momentum: float | None, dtype: str = F32, fused: bool = True,
+        weight_decay: float = 0.0, nesterov: bool = False):
     """A trajectory: ``schedule[t] = (active, groups)``; ``grad_fn(t)`` returns
     the (N, P) stored gradients of step t.  Returns final (param, mom)."""
     p, v = param0, mom0
     for t, (active, groups) in enumerate(schedule):
-        p, v = step(p, grad_fn(t), v, groups, active, lr, momentum, dtype, fused)
+        p, v = step(p, grad_fn(t), v, groups, active, lr, momentum, dtype, fused,
+                    weight_decay, nesterov)
     return p, v

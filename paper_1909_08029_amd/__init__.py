@@ -61,7 +61,8 @@ class WorkerState(ctypes.Structure):
 
 
 class Sgd(ctypes.Structure):
-    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float)]
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("nesterov", ctypes.c_int32)]
 
 
 def _load():
@@ -255,21 +256,23 @@ def _stream_ptr(stream) -> Optional[int]:
 
 
 def rip_local_step(rep: Replicas, active: Sequence[int], lr: float, momentum: float = 0.0,
-                   stream=None) -> None:
+                   stream=None, weight_decay: float = 0.0, nesterov: bool = False) -> None:
     """Step 2 of Fig. 4 for the listed workers (see include/rip.h)."""
     act = _i32_array(list(active))
-    sgd = Sgd(lr, momentum)
+    sgd = Sgd(lr, momentum, weight_decay, int(bool(nesterov)))
     _check(lib.rip_local_step(rep._h, act, len(active), ctypes.byref(sgd),
                               _stream_ptr(stream)))
 
 
 def rip_preduce(rep: Replicas, groups: Sequence[Sequence[int]], active: Sequence[int] = (),
-                lr: Optional[float] = None, momentum: float = 0.0, stream=None) -> None:
+                lr: Optional[float] = None, momentum: float = 0.0, stream=None,
+                weight_decay: float = 0.0, nesterov: bool = False) -> None:
     """Fused local update of ``active`` and P-Reduce of the disjoint ``groups``
     in one launch (see include/rip.h).  ``lr=None`` is pure P-Reduce."""
     off, mem = _csr(groups)
     act = _i32_array(list(active))
-    sgd = None if lr is None else ctypes.byref(Sgd(lr, momentum))
+    sgd = None if lr is None else ctypes.byref(
+        Sgd(lr, momentum, weight_decay, int(bool(nesterov))))
     _check(lib.rip_preduce(rep._h, off, mem, len(groups), act, len(active), sgd,
                            _stream_ptr(stream)))
 

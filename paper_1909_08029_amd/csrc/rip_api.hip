@@ -242,6 +242,8 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
     if (sgd->momentum != 0.0f && !r->has_mom)
       return rip::fail(RIP_E_INVAL, "momentum %g without momentum buffers", (double)sgd->momentum);
   }
+  if (sgd && sgd->nesterov && sgd->momentum == 0.0f)
+    return rip::fail(RIP_E_INVAL, "Nesterov momentum needs a nonzero momentum");
   std::vector<uint8_t> in_group(N, 0), is_active(N, 0);
   for (int32_t i = 0; i < n_active; ++i) {
     const int32_t id = active[i];
@@ -289,6 +291,8 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
   a.n_units = units;
   a.lr = sgd ? sgd->lr : 0.0f;
   a.mu = sgd ? sgd->momentum : 0.0f;
+  a.wd = sgd ? sgd->weight_decay : 0.0f;
+  a.nesterov = sgd && sgd->nesterov ? 1 : 0;
   mom = sgd && sgd->momentum != 0.0f && n_active > 0;
   int64_t work = 0;
   a.unit_work0[0] = 0;

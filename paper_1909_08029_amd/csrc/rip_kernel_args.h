@@ -42,7 +42,8 @@ struct StepArgs {
                               // segment, for tiles of 1, 2, 4, 8 slots
   int32_t n_seg, n_rep, n_units;
   uint32_t work;              // work items (tiles) of all units
-  float lr, mu;
+  float lr, mu, wd;
+  int32_t nesterov;
   uint32_t unit_work0[RIP_MAX_REPLICAS + 1];  // first work item of each unit
   uint16_t unit_off[RIP_MAX_REPLICAS + 1];    // unit u = member[unit_off[u] .. unit_off[u+1])
   uint16_t member[RIP_MAX_REPLICAS];          // replica ids, ascending within a unit

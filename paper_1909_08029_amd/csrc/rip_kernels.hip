@@ -157,6 +157,27 @@ constexpr InvTable make_inv_table() {
 }
 __constant__ InvTable kInv = make_inv_table();
 
+// Step 2 for one element (fp32, this order, no contraction):
+//   g' = g + wd*w                       (only when weight decay is on)
+//   SGD:       u = w - lr*g'
+//   momentum:  v = mu*v + g';  u = w - lr*v,  or with Nesterov u = w - lr*(g' + mu*v)
+// wd and nesterov are wave-uniform, so their tests are scalar branches.
+struct Opt {
+  float lr, mu, wd;
+  bool nesterov;
+};
+
+template <bool MOM>
+__device__ __forceinline__ float update(float w, float g, float& v, const Opt& o) {
+  if (o.wd != 0.0f) g = g + o.wd * w;
+  if constexpr (MOM) {
+    v = o.mu * v + g;
+    return w - o.lr * (o.nesterov ? g + o.mu * v : v);
+  } else {
+    return w - o.lr * g;
+  }
+}
+
 struct Members {
   char* w[kMaxK];
   const char* g[kMaxK];
@@ -180,8 +201,8 @@ __device__ __forceinline__ void load_members(const StepArgs& a, int base, int se
 
 // U consecutive 16-byte slots of a full tile for a unit of K members.
 template <int K, int U, bool BF16, bool MOM>
-__device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off)[U], float lr,
-                                           float mu) {
+__device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off)[U],
+                                           const Opt& o) {
   using V = Vec<BF16>;
   constexpr int N = V::N;
   constexpr float inv_k = (float)(1.0 / K);
@@ -204,21 +225,12 @@ __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off
       float x[N];
       V::unpack(wv[u][j], x);
       if (m.act[j]) {
-        float g[N];
+        float g[N], v[N];
         V::unpack(gv[u][j], g);
-        if constexpr (MOM) {
-          float v[N];
-          V::unpack(vv[u][j], v);
+        if constexpr (MOM) V::unpack(vv[u][j], v);
 #pragma unroll
-          for (int i = 0; i < N; ++i) {
-            v[i] = mu * v[i] + g[i];
-            x[i] = x[i] - lr * v[i];
-          }
-          st16(m.v[j] + off[u], V::pack(v));
-        } else {
-#pragma unroll
-          for (int i = 0; i < N; ++i) x[i] = x[i] - lr * g[i];
-        }
+        for (int i = 0; i < N; ++i) x[i] = update<MOM>(x[i], g[i], v[i], o);
+        if constexpr (MOM) st16(m.v[j] + off[u], V::pack(v));
       }
 #pragma unroll
       for (int i = 0; i < N; ++i) s[i] = (j == 0) ? x[i] : s[i] + x[i];
@@ -240,6 +252,7 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
                             int64_t end) {
   const int plane = a.n_seg * a.n_rep;
   const float inv_k = kInv.v[k];
+  const Opt o{a.lr, a.mu, a.wd, a.nesterov != 0};
   for (int64_t e = begin + threadIdx.x; e < end; e += kBlock) {
     float s = 0.0f;
     for (int j = 0; j < k; ++j) {
@@ -251,11 +264,12 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
         const float g = ld1<BF16>(reinterpret_cast<const char*>(a.ptab[plane + idx]), e);
         if constexpr (MOM) {
           char* vp = reinterpret_cast<char*>(a.ptab[2 * plane + idx]);
-          const float v = a.mu * ld1<BF16>(vp, e) + g;
+          float v = ld1<BF16>(vp, e);
+          x = update<true>(x, g, v, o);
           st1<BF16>(vp, e, v);
-          x = x - a.lr * v;
         } else {
-          x = x - a.lr * g;
+          float unused = 0.0f;
+          x = update<false>(x, g, unused, o);
         }
       }
       s = (j == 0) ? x : s + x;
@@ -279,7 +293,7 @@ __device__ __forceinline__ void full_tile(const StepArgs& a, int base, int seg, 
 #pragma unroll
   for (int u = 0; u < SL; ++u)
     off[u] = (e_tile + (int64_t)(u * kBlock + (int)threadIdx.x) * N) * esize;
-  tile_slots<K, SL, BF16, MOM>(m, off, a.lr, a.mu);
+  tile_slots<K, SL, BF16, MOM>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
 }
 
 // Last index i in [0, n) with v[i] <= x (v ascending, v[0] <= x).

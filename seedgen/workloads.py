@@ -53,6 +53,8 @@ class Workload:
     param_sigma: float = 1.0
     grad_ring: int = 2
     note: str = ""
+    weight_decay: float = 0.0
+    nesterov: bool = False
 
     @property
     def numel(self) -> int:

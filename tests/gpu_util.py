@@ -75,11 +75,12 @@ class GpuRun:
         w = self.w
         active, groups = rip.rip_schedule_groups(self.sched, self.t, w.eligible(self.t))
         h = self.handles[w.grad_slot(self.t)]
+        opt = dict(weight_decay=w.weight_decay, nesterov=w.nesterov)
         if self.fused:
-            rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum)
+            rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, **opt)
         else:
             if active:
-                rip.rip_local_step(h, active, w.lr, w.momentum)
+                rip.rip_local_step(h, active, w.lr, w.momentum, **opt)
             rip.rip_preduce(h, groups)
         self.schedule.append((active, groups))
         self.t += 1
@@ -99,7 +100,8 @@ def oracle_windows(w: wl.Workload, schedule, windows: Sequence[Tuple[int, int]],
         p, grad, v = wl.host_inputs(w, a, b)
         for t, (active, groups) in enumerate(schedule):
             p, v = op.step(p, grad(w.grad_slot(t)), v, groups, active, w.lr,
-                           w.momentum if w.momentum else None, dt, fused)
+                           w.momentum if w.momentum else None, dt, fused,
+                           w.weight_decay, w.nesterov)
         out.append((p, v))
     return out
 

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(rip.LIB_PATH)
     for name in names:
         assert hasattr(lib, name), f"{name} declared in rip.h but not exported"
-    assert rip.abi_version() == 1
+    assert rip.abi_version() == 2
 
 
 def _straggler(n, t, every):
@@ -150,5 +150,5 @@ def test_replicas_create_checks_before_any_device_call():
         rip.RIP_E_INVAL
     assert b"NULL" in lib.rip_last_error()
     assert lib.rip_preduce(None, None, None, 0, None, 0, None, None) == rip.RIP_E_INVAL
-    sgd = rip.Sgd(0.1, 0.0)
+    sgd = rip.Sgd(0.1, 0.0, 0.0, 0)
     assert lib.rip_local_step(None, None, 0, ctypes.byref(sgd), None) == rip.RIP_E_INVAL

@@ -108,6 +108,40 @@ def test_unfused_local_step_then_preduce(dtype):
     check_against_oracle(run, full_windows(w.numel), "unfused")
 
 
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+@pytest.mark.parametrize("wd,nesterov,mom,fused", [
+    (1e-4, False, 0.9, True),      # the paper's ResNet-50 optimizer
+    (1e-2, True, 0.9, True),
+    (5e-3, False, 0.0, True),
+    (0.0, True, 0.5, True),
+    (1e-2, True, 0.9, False),
+])
+def test_optimizer_variants(dtype, wd, nesterov, mom, fused):
+    """Weight decay and Nesterov momentum, fused and unfused, on random
+    groups with a straggler (so groups also hold members that did not
+    update this step)."""
+    w = wl.scaled(wl.CONFIGS[3], [3 * 4096 + 11, 777], steps=8, n=8, dtype=dtype,
+                  lr=0.1 if dtype == DTYPE_F32 else 20.0, momentum=mom, weight_decay=wd,
+                  nesterov=nesterov, sched=dict(mode=wl.RANDOM_GB, seed=9, kmin=2, kmax=8),
+                  straggler_every=3, grad_ring=3)
+    log(f"case optimizer dtype={dtype} wd={wd} nesterov={nesterov} mom={mom} fused={fused}")
+    run = GpuRun(w, "separate", fused=fused)
+    run.run(w.steps)
+    check_against_oracle(run, full_windows(w.numel), "optimizer")
+
+
+def test_nesterov_without_momentum_is_rejected():
+    import paper_1909_08029_amd as rip
+    w = wl.Workload("nest", 2, [4096], DTYPE_F32, 0.1, 0.0, 0.01,
+                    dict(mode=wl.TABLE, table=[[(0, 1)]]), 1, 71, grad_ring=1)
+    st = wl.DeviceState(w)
+    st.fill()
+    h = rip.Replicas(st.param, st.grad_sets[0], None)
+    with pytest.raises(rip.RipError) as e:
+        rip.rip_preduce(h, [(0, 1)], [0, 1], lr=0.1, nesterov=True)
+    assert e.value.code == rip.RIP_E_INVAL
+
+
 def test_random_gb_straggler_small():
     w = wl.scaled(wl.CONFIGS[4], [3 * 4096 + 17], steps=40)
     log("case random-gb small")

@@ -25,6 +25,8 @@ PRE_PINS = [
     (tp.test_conflict_worked_example, ()),
     (tp.test_sgd_closed_form, ()),
     (tp.test_momentum_closed_form, ()),
+    (tp.test_weight_decay_closed_form, ()),
+    (tp.test_nesterov_closed_form, ()),
     (tp.test_step_against_float64_definition, ()),
     (tp.test_bf16_step_rounds_once, ()),
     (tp.test_bf16_rounding_matches_torch, ()),
@@ -85,23 +87,31 @@ def mean_wrong_divisor(values):
     return s * op.inv_k(k + 1)
 
 
-def update_sign_flip(w, g, v, lr, momentum):
-    u, v2 = ORIG_UPDATE(w, g, v, lr, momentum)
+def update_sign_flip(w, g, v, lr, momentum, wd=0.0, nesterov=False):
+    u, v2 = ORIG_UPDATE(w, g, v, lr, momentum, wd, nesterov)
     return w + (w - u), v2
 
 
-def update_lr_inside_momentum(w, g, v, lr, momentum):
+def update_lr_inside_momentum(w, g, v, lr, momentum, wd=0.0, nesterov=False):
     if momentum is None:
-        return ORIG_UPDATE(w, g, v, lr, momentum)
+        return ORIG_UPDATE(w, g, v, lr, momentum, wd, nesterov)
     v_new = np.float32(momentum) * v + np.float32(lr) * g
     return w - v_new, v_new
 
 
-def update_uses_old_velocity(w, g, v, lr, momentum):
+def update_uses_old_velocity(w, g, v, lr, momentum, wd=0.0, nesterov=False):
     if momentum is None:
-        return ORIG_UPDATE(w, g, v, lr, momentum)
+        return ORIG_UPDATE(w, g, v, lr, momentum, wd, nesterov)
     v_new = np.float32(momentum) * v + g
     return w - np.float32(lr) * v, v_new
+
+
+def update_decay_sign_flipped(w, g, v, lr, momentum, wd=0.0, nesterov=False):
+    return ORIG_UPDATE(w, g, v, lr, momentum, -wd, nesterov)
+
+
+def update_ignores_nesterov(w, g, v, lr, momentum, wd=0.0, nesterov=False):
+    return ORIG_UPDATE(w, g, v, lr, momentum, wd, False)
 
 
 def bf16_truncate(x):
@@ -119,10 +129,11 @@ ORIG_STEP = op.step
 
 
 def step_updates_every_member(param, grad, mom, groups, active, lr=0.0, momentum=None,
-                              dtype=op.F32, fused=True):
+                              dtype=op.F32, fused=True, weight_decay=0.0, nesterov=False):
     if grad is not None:
         active = sorted(set(active) | {m for g in groups for m in g})
-    return ORIG_STEP(param, grad, mom, groups, active, lr, momentum, dtype, fused)
+    return ORIG_STEP(param, grad, mom, groups, active, lr, momentum, dtype, fused,
+                     weight_decay, nesterov)
 
 
 ARITH = [
@@ -132,6 +143,8 @@ ARITH = [
     ("update sign flipped", "local_update", update_sign_flip),
     ("lr folded into the velocity", "local_update", update_lr_inside_momentum),
     ("update uses the old velocity", "local_update", update_uses_old_velocity),
+    ("weight decay sign flipped", "local_update", update_decay_sign_flipped),
+    ("Nesterov look-ahead ignored", "local_update", update_ignores_nesterov),
     ("bf16 truncates", "f32_to_bf16", bf16_truncate),
     ("bf16 rounds ties away from zero", "f32_to_bf16", bf16_ties_away),
     ("update applied to every group member", "step", step_updates_every_member),

@@ -308,3 +308,44 @@ def test_schedule_validation():
         op.preduce(X, [(2, 1)])
     with pytest.raises(ValueError):
         op.preduce(X, [(0, 4)])
+
+
+def test_weight_decay_closed_form():
+    # SGD with weight decay and constant g: w_{t+1} = (1 - lr*wd) w_t - lr*g,
+    # so w_T = (w_0 + g/wd) (1 - lr*wd)^T - g/wd.
+    rs = np.random.default_rng(12)
+    n, p, T, lr, wd = 2, 4096, 40, 0.1, 1e-2
+    W = rng_f32(rs, (n, p))
+    W0 = W.copy()
+    G = rng_f32(rs, (n, p), 0.01)
+    for _ in range(T):
+        W, _ = op.step(W, G, None, [], range(n), lr=lr, weight_decay=wd)
+    lr64, wd64 = np.float64(np.float32(lr)), np.float64(np.float32(wd))
+    a = 1 - lr64 * wd64
+    G64 = G.astype(np.float64)
+    exact = (W0.astype(np.float64) + G64 / wd64) * a ** T - G64 / wd64
+    assert np.all(np.abs(W - exact) <= 4 * T * U32 * (np.abs(W0) + T * lr * np.abs(G)))
+    # dropping the decay term moves w by about T*lr*wd*|w|, far outside the bound
+    W_nodecay = W0 - np.float32(T * lr) * G
+    assert np.max(np.abs(W_nodecay - exact)) > 100 * np.max(4 * T * U32 * np.abs(W0))
+
+
+def test_nesterov_closed_form():
+    # v_t = g (1 - mu^t)/(1 - mu); Nesterov step d_t = g + mu v_t;
+    # w_T = w_0 - lr * sum_{t=1..T} d_t.
+    rs = np.random.default_rng(13)
+    n, p, T, lr, mu = 2, 4096, 30, 0.1, 0.9
+    W = rng_f32(rs, (n, p))
+    W0 = W.copy()
+    G = rng_f32(rs, (n, p), 0.01)
+    V = np.zeros_like(W)
+    for _ in range(T):
+        W, V = op.step(W, G, V, [], range(n), lr=lr, momentum=mu, nesterov=True)
+    mu64, lr64 = np.float64(np.float32(mu)), np.float64(np.float32(lr))
+    G64 = G.astype(np.float64)
+    coef = sum(1 + mu64 * (1 - mu64 ** t) / (1 - mu64) for t in range(1, T + 1))
+    exact = W0.astype(np.float64) - lr64 * G64 * coef
+    assert np.all(np.abs(W - exact) <= 6 * T * U32 * (np.abs(W0) + lr * coef * np.abs(G)))
+    # heavy-ball (no look-ahead) ends elsewhere: sum of v_t differs from sum of d_t
+    coef_hb = sum((1 - mu64 ** t) / (1 - mu64) for t in range(1, T + 1))
+    assert abs(coef - coef_hb) > 1.0
