@@ -74,19 +74,20 @@ int32_t rip_abi_version(void);
  *       TABLE / STATIC / RULE: the group of row (c_i - 1) mod period that
  *         contains it (a static schedule, Sec. 4.2, Fig. 8, Fig. 9); a worker
  *         with no group in that row skips synchronization (Sec. 4.2);
- *       RANDOM_GB / GD / SCRIPTED: the head of its Group Buffer if that is
- *         not empty; else new groups are made and appended to the buffer of
- *         every member: one random group containing it (RANDOM_GB, Step 3 of
- *         Fig. 4), a random partition of all idle workers (Global Division,
- *         Sec. 5.1) admitting only workers w with c_i - c_w < c_thres when
- *         c_thres > 0 (Sec. 5.3), or the next group of a caller's script.
+ *       RANDOM_GB / GD / INTER_INTRA / SCRIPTED: the head of its Group
+ *         Buffer if that is not empty; else new groups are made and appended
+ *         to the buffer of every member: one random group containing it
+ *         (RANDOM_GB, Step 3 of Fig. 4), a random partition of all idle
+ *         workers (Global Division, Sec. 5.1) admitting only workers w with
+ *         c_i - c_w < c_thres when c_thres > 0 (Sec. 5.3), the two-phase
+ *         Inter-Intra division (Sec. 5.2), or the next group of a script.
  *  3. A group runs when it heads every member's buffer and every member is
  *     blocked in it (serialization of conflicting groups, Sec. 4.1).  The
  *     groups that run are therefore disjoint.  Their members unblock.
  *
  * Random draws: SplitMix64 (Steele, Lea & Flood 2014) with keys folded as
  * k <- mix(k + 0x9E3779B97F4A7C15*(c+1)); bounded(n) = ((x>>32)*n)>>32.
- *   RANDOM_GB/GD: one sequential stream from fold(seed, 3).
+ *   RANDOM_GB/GD/INTER_INTRA: one sequential stream from fold(seed, 3).
  *     RANDOM_GB group: k = min(kmin + bounded(kmax-kmin+1), N); the other
  *     k-1 members by a partial Fisher-Yates over the ascending ids != i
  *     (slot j swaps with j + bounded(N-1-j)).
@@ -99,6 +100,13 @@ int32_t rip_abi_version(void);
  *     workers (the spectral-gap condition of Sec. 3.3); at most 1000.
  *   RULE: the rule table of Fig. 9: n_nodes nodes of 4 local workers, rank
  *     node*4 + local, period 4 (n_nodes = 1 or even).
+ *   INTER_INTRA (Sec. 5.2): N/n_nodes consecutive workers per node.  A
+ *     worker with an empty buffer divides the idle workers (same filter as
+ *     GD): per node in ascending order a head = idle[bounded(count)]; the
+ *     heads (ascending node order), then each node's other idle workers, are
+ *     Fisher-Yates shuffled and cut into chunks as in GD (inter phase); then
+ *     each node's idle workers form one group (intra phase).  Every idle
+ *     worker thus gets its inter group, then its intra group, in its buffer.
  * ---------------------------------------------------------------------- */
 enum {
   RIP_SCHED_TABLE = 0,      /* caller's periodic table (FIXED = one row)   */
@@ -106,7 +114,8 @@ enum {
   RIP_SCHED_RANDOM_GB = 2,  /* random group per request + Group Buffers    */
   RIP_SCHED_GD = 3,         /* Global Division (+ slowdown filter)         */
   RIP_SCHED_SCRIPTED = 4,   /* Group Buffers fed by a caller's group list  */
-  RIP_SCHED_RULE = 5        /* the rule table of Fig. 9                    */
+  RIP_SCHED_RULE = 5,       /* the rule table of Fig. 9                    */
+  RIP_SCHED_INTER_INTRA = 6 /* Inter-Intra division (Sec. 5.2)             */
 };
 
 typedef struct rip_sched rip_sched; /* opaque, library-owned */
@@ -114,12 +123,12 @@ typedef struct rip_sched rip_sched; /* opaque, library-owned */
 typedef struct rip_sched_cfg {
   int32_t n_workers;   /* N, 1..RIP_MAX_REPLICAS */
   int32_t mode;        /* RIP_SCHED_* */
-  uint64_t seed;       /* STATIC, RANDOM_GB, GD */
+  uint64_t seed;       /* STATIC, RANDOM_GB, GD, INTER_INTRA */
   int32_t group_size;  /* STATIC: N % group_size == 0, group_size >= 2 if N > 1 */
   int32_t period;      /* STATIC: rows per period (>= 1); TABLE: number of rows */
-  int32_t kmin, kmax;  /* RANDOM_GB, GD: 1 <= kmin <= kmax */
-  int32_t c_thres;     /* GD: slowdown threshold, <= 0 disables the filter */
-  int32_t n_nodes;     /* RULE: N == 4 * n_nodes */
+  int32_t kmin, kmax;  /* RANDOM_GB, GD, INTER_INTRA: 1 <= kmin <= kmax */
+  int32_t c_thres;     /* GD, INTER_INTRA: slowdown threshold, <= 0 = off */
+  int32_t n_nodes;     /* RULE: N == 4 * n_nodes; INTER_INTRA: N % n_nodes == 0 */
   /* TABLE: row r holds groups row_offsets[r] .. row_offsets[r+1]-1;
    * SCRIPTED: groups 0 .. n_groups-1 handed out in order.
    * Group g has members members[group_offsets[g] .. group_offsets[g+1]-1],

@@ -27,7 +27,8 @@ One step t:
          Fig. 4 with the buffer of Sec. 5.1), or a random partition of every
          idle worker (empty buffer) into groups (Global Division, Sec. 5.1),
          optionally keeping only workers whose counter is within C_thres of
-         the initiator's (Sec. 5.3), or the next group of a fixed script.
+         the initiator's (Sec. 5.3), the two-phase Inter-Intra division of
+         Sec. 5.2, or the next group of a fixed script.
   3. A group executes when it is the head of every member's buffer and every
      member is waiting (the lock-vector rule of Sec. 4.1: overlapping groups
      run one after the other, in creation order).  Executed groups are
@@ -53,6 +54,7 @@ RANDOM_GB = 2
 GD = 3
 SCRIPTED = 4
 RULE = 5
+INTER_INTRA = 6
 
 SCHED_TAG = 3
 MAX_STATIC_ATTEMPTS = 1000
@@ -160,9 +162,12 @@ class Scheduler:
             if n != 4 * n_nodes:
                 raise ValueError("rule table needs n == 4 * n_nodes")
             self.rows = rule_table(n_nodes)
-        elif mode in (RANDOM_GB, GD):
+        elif mode in (RANDOM_GB, GD, INTER_INTRA):
             if not 1 <= kmin <= kmax:
                 raise ValueError("need 1 <= kmin <= kmax")
+            if mode == INTER_INTRA and (n_nodes < 1 or n % n_nodes != 0):
+                raise ValueError("inter-intra needs n % n_nodes == 0")
+            self.per_node = n // n_nodes if n_nodes else 0
             self.rng = Stream(fold(seed, SCHED_TAG))
         elif mode == SCRIPTED:
             self.script = [tuple(g) for g in script]
@@ -210,6 +215,43 @@ class Scheduler:
             pos += k
         self.divisions.append((i, list(self.c), made))
 
+    def _chunks(self, members):
+        """Fisher-Yates shuffle, then consecutive chunks of drawn sizes."""
+        members = list(members)
+        for a in range(len(members) - 1, 0, -1):
+            b = self.rng.bounded(a + 1)
+            members[a], members[b] = members[b], members[a]
+        pos, out = 0, []
+        while pos < len(members):
+            k = self.kmin + self.rng.bounded(self.kmax - self.kmin + 1)
+            out.append(members[pos:pos + k])
+            pos += k
+        return out
+
+    def _inter_intra_division(self, i: int):
+        """Inter-Intra synchronization (Sec. 5.2) as a division of the idle
+        workers: each gets two buffer entries, an inter-phase group (one head
+        per node, chosen at random among the node's idle workers, heads
+        grouped across nodes; the other idle workers grouped within their
+        node), then an intra-phase group (every idle worker of its node)."""
+        idle = [w for w in range(self.n) if not self.gb[w] and
+                (self.c_thres <= 0 or self.c[i] - self.c[w] < self.c_thres)]
+        nodes = {}
+        for w in idle:
+            nodes.setdefault(w // self.per_node, []).append(w)
+        heads, locals_ = [], {}
+        for nd in sorted(nodes):
+            ws = nodes[nd]
+            h = ws[self.rng.bounded(len(ws))]
+            heads.append(h)
+            locals_[nd] = [w for w in ws if w != h]
+        made = [self.groups[self._new_group(g)] for g in self._chunks(heads)]
+        for nd in sorted(nodes):
+            made += [self.groups[self._new_group(g)] for g in self._chunks(locals_[nd])]
+        for nd in sorted(nodes):
+            made.append(self.groups[self._new_group(nodes[nd])])
+        self.divisions.append((i, list(self.c), made))
+
     def _scripted_group(self, i: int):
         if self.script_pos >= len(self.script):
             raise ValueError("script exhausted")
@@ -239,6 +281,8 @@ class Scheduler:
                 self._random_group(i)
             elif self.mode == GD:
                 self._global_division(i)
+            elif self.mode == INTER_INTRA:
+                self._inter_intra_division(i)
             else:
                 self._scripted_group(i)
         self.waiting[i] = True

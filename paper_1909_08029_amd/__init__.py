@@ -33,6 +33,7 @@ SCHED_RANDOM_GB = 2
 SCHED_GD = 3
 SCHED_SCRIPTED = 4
 SCHED_RULE = 5
+SCHED_INTER_INTRA = 6
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
 

@@ -125,6 +125,7 @@ bool valid_group(const int32_t* m, int32_t len, int n) {
 struct rip_sched {
   int n = 0, mode = 0;
   int kmin = 0, kmax = 0, c_thres = 0;
+  int per_node = 1;  // INTER_INTRA: workers per node
   // evolving state (copied as a whole to make a failed step a no-op)
   struct State {
     int64_t t = 0;
@@ -179,6 +180,44 @@ struct rip_sched {
     }
   }
 
+  // Fisher-Yates shuffle of `m`, then consecutive chunks of drawn sizes.
+  std::vector<Group> chunks(std::vector<int32_t> m) {
+    for (int a = (int)m.size() - 1; a >= 1; --a) std::swap(m[a], m[st.rng.bounded((uint32_t)a + 1)]);
+    std::vector<Group> out;
+    size_t pos = 0;
+    while (pos < m.size()) {
+      const size_t k = (size_t)(kmin + st.rng.bounded((uint32_t)(kmax - kmin + 1)));
+      const size_t end = std::min(m.size(), pos + k);
+      out.emplace_back(m.begin() + pos, m.begin() + end);
+      pos = end;
+    }
+    return out;
+  }
+
+  // Inter-Intra synchronization (Sec. 5.2) as one division of the idle
+  // workers: an inter-phase group for each (a random head per node, heads
+  // grouped across nodes; the rest grouped within their node), then an
+  // intra-phase group of every idle worker of the node.
+  void inter_intra_division(int i) {
+    std::map<int, std::vector<int32_t>> nodes;  // ascending node id
+    for (int w = 0; w < n; ++w)
+      if (st.gb[w].empty() && (c_thres <= 0 || st.c[i] - st.c[w] < c_thres))
+        nodes[w / per_node].push_back(w);
+    std::vector<int32_t> heads;
+    std::map<int, std::vector<int32_t>> rest;
+    for (auto& [nd, ws] : nodes) {
+      const int32_t h = ws[st.rng.bounded((uint32_t)ws.size())];
+      heads.push_back(h);
+      for (int32_t w : ws)
+        if (w != h) rest[nd].push_back(w);
+      rest[nd];  // a node whose only idle worker is its head has no local groups
+    }
+    for (Group& g : chunks(heads)) new_group(std::move(g));
+    for (auto& [nd, ws] : rest)
+      for (Group& g : chunks(ws)) new_group(std::move(g));
+    for (auto& [nd, ws] : nodes) new_group(ws);
+  }
+
   int32_t request(int i) {
     st.c[i] += 1;
     if (table_mode()) {
@@ -201,6 +240,8 @@ struct rip_sched {
         random_group(i);
       } else if (mode == RIP_SCHED_GD) {
         global_division(i);
+      } else if (mode == RIP_SCHED_INTER_INTRA) {
+        inter_intra_division(i);
       } else {
         if (st.script_pos >= script.size())
           return rip::fail(RIP_E_INVAL, "scripted group list exhausted at worker %d", i);
@@ -293,10 +334,18 @@ extern "C" int32_t rip_sched_create(const rip_sched_cfg* cfg, rip_sched** out) {
       break;
     }
     case RIP_SCHED_RANDOM_GB:
-    case RIP_SCHED_GD: {
+    case RIP_SCHED_GD:
+    case RIP_SCHED_INTER_INTRA: {
       if (cfg->kmin < 1 || cfg->kmax < cfg->kmin) {
         rc = rip::fail(RIP_E_INVAL, "need 1 <= kmin <= kmax");
         break;
+      }
+      if (cfg->mode == RIP_SCHED_INTER_INTRA) {
+        if (cfg->n_nodes < 1 || n % cfg->n_nodes != 0) {
+          rc = rip::fail(RIP_E_INVAL, "INTER_INTRA needs N %% n_nodes == 0");
+          break;
+        }
+        s->per_node = n / cfg->n_nodes;
       }
       s->kmin = cfg->kmin;
       s->kmax = cfg->kmax;

@@ -54,6 +54,10 @@ CASES = [
     (32, dict(mode=os_.GD, seed=9, kmin=3, kmax=3, c_thres=3),
      dict(mode=rip.SCHED_GD, seed=9, kmin=3, kmax=3, c_thres=3), 5),
     (16, dict(mode=os_.RULE, n_nodes=4), dict(mode=rip.SCHED_RULE, n_nodes=4), 3),
+    (32, dict(mode=os_.INTER_INTRA, seed=6, kmin=2, kmax=4, n_nodes=4),
+     dict(mode=rip.SCHED_INTER_INTRA, seed=6, kmin=2, kmax=4, n_nodes=4), 4),
+    (24, dict(mode=os_.INTER_INTRA, seed=7, kmin=1, kmax=3, c_thres=2, n_nodes=3),
+     dict(mode=rip.SCHED_INTER_INTRA, seed=7, kmin=1, kmax=3, c_thres=2, n_nodes=3), 3),
     (7, dict(mode=os_.RANDOM_GB, seed=2 ** 64 - 1, kmin=1, kmax=9),
      dict(mode=rip.SCHED_RANDOM_GB, seed=2 ** 64 - 1, kmin=1, kmax=9), 2),
     (12, dict(mode=os_.TABLE, table=[[(0, 5), (1, 2, 3)], [], [(4, 6, 7, 8, 9, 10, 11)]]),

@@ -213,6 +213,46 @@ def test_slowdown_filter_rule():
     assert full(s) >= n - 2 > full(nofilter)
 
 
+@pytest.mark.parametrize("n,nodes,kmin,kmax", [(16, 4, 2, 3), (32, 4, 2, 8), (12, 3, 1, 2)])
+def test_inter_intra_division(n, nodes, kmin, kmax):
+    """Sec. 5.2: a division gives every idle worker two buffered groups.  The
+    inter-phase group is either a group of head workers (at most one per
+    node, one head per node in all) or a group of one node's non-head
+    workers; the intra-phase group is every idle worker of the node."""
+    per = n // nodes
+    s = os_.Scheduler(n, os_.INTER_INTRA, seed=5, kmin=kmin, kmax=kmax, n_nodes=nodes)
+    s.step(0, [i == 0 for i in range(n)])          # only worker 0 asks: all others idle
+    i, c, made = s.divisions[0]
+    node = lambda w: w // per
+    intra = made[-nodes:]
+    inter = made[:-nodes]
+    assert sorted(intra) == [tuple(range(nd * per, nd * per + per)) for nd in range(nodes)]
+    assert sorted(m for g in inter for m in g) == list(range(n))
+    heads = set()
+    for g in inter:
+        if len({node(m) for m in g}) > 1:
+            heads |= set(g)
+    # each multi-node group holds at most one worker per node
+    for g in inter:
+        nds = [node(m) for m in g]
+        assert len(nds) == len(set(nds)) or len(set(nds)) == 1
+    assert len({node(h) for h in heads}) == len(heads)
+    for w in range(n):
+        # worker 0's inter group may already have run (if it was alone)
+        assert len(s.gb[w]) == (2 if w != 0 else len(s.gb[w]))
+        assert s.groups[s.gb[w][-1]] == tuple(range(node(w) * per, node(w) * per + per))
+    # run on: every worker alternates inter and intra phases; all stay served
+    for t in range(1, 200):
+        act, groups = s.step(t)
+        check_step_invariants(s, act, groups, n)
+    assert min(s.syncs) > 50
+
+
+def test_inter_intra_rejects_uneven_nodes():
+    with pytest.raises(ValueError):
+        os_.Scheduler(10, os_.INTER_INTRA, kmin=2, kmax=2, n_nodes=4)
+
+
 def test_steps_must_be_consecutive():
     s = os_.Scheduler(4, os_.RANDOM_GB, seed=0, kmin=2, kmax=2)
     s.step(0)
