@@ -48,9 +48,12 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str):
-    """HBM bytes per launch measured with rocprofv3 counters, if they were
-    taken on the current kernel source for this workload."""
+def load_traffic(workload: str, alg_bytes_per_launch: float):
+    """HBM bytes per launch from the rocprofv3 FETCH_SIZE/WRITE_SIZE passes
+    (scaled by a copy of known size), if they were taken on the current
+    kernel source for this workload: the measured traffic/algorithmic ratio
+    times this run's algorithmic bytes per launch (the two agree for
+    workloads whose launches all move the same bytes)."""
     try:
         with open(TRAFFIC_FILE) as f:
             data = json.load(f)
@@ -59,7 +62,7 @@ def load_traffic(workload: str):
     ent = data.get(workload)
     if not ent or ent.get("kernel_hash") != kernel_hash():
         return None
-    return ent.get("traffic_bytes_per_launch")
+    return int(round(ent["traffic_over_alg"] * alg_bytes_per_launch))
 
 
 def cpu_baseline(w, seconds: float = 12.0):
@@ -202,7 +205,9 @@ def main():
     mean_launch_bytes = sum(b for b, _ in launched) / max(1, len(launched))
     mean_kernel_ms = sum(ms for _, ms in launched) / max(1, len(launched))
     achieved = mean_launch_bytes / (mean_kernel_ms * 1e-3) / 1e9 if launched else 0.0
-    traffic = load_traffic(w.name + ("" if args.layout == "flat" else "_separate"))
+    traffic = None
+    if args.layout == "flat" and not args.grad_ring:
+        traffic = load_traffic(w.name, mean_launch_bytes)
 
     cpu = None
     if not args.no_cpu_baseline:

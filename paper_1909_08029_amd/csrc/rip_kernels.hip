@@ -12,8 +12,8 @@
 // unit's number of streams grows (see slot_log2), so every wave keeps about
 // 24 16-byte loads in flight per lane whatever the group size.  The host caps
 // residency at 8-10 waves per CU (an LDS reservation): HBM3E delivered its
-// best rate at that depth of outstanding requests, not at full occupancy.  A workgroup
-// handles one unit, so the unit's size k, its member ids and their active
+// best rate at that depth of outstanding requests, not at full occupancy.
+// A workgroup handles one unit, so the unit's size k, its member ids and their active
 // flags are wave-uniform: they sit in scalar registers and every branch on
 // them is a scalar branch.  Each thread issues the loads of all members
 // (and their gradients / momenta) for all its slots before any arithmetic,
