@@ -107,6 +107,14 @@ int32_t rip_abi_version(void);
  *     Fisher-Yates shuffled and cut into chunks as in GD (inter phase); then
  *     each node's idle workers form one group (intra phase).  Every idle
  *     worker thus gets its inter group, then its intra group, in its buffer.
+ *   ADPSGD (the baseline of Fig. 3, for comparison on the same kernel): each
+ *     active worker i draws x = bounded(N-1) and pairs with j = x (x < i) or
+ *     x + 1; j is passive and need not be waiting.  Waiting requesters are
+ *     then served oldest first; a pair runs unless one of its two workers
+ *     is already in a pair of this step (the atomic averaging of Fig. 3),
+ *     otherwise the requester keeps waiting.  Groups come out in request
+ *     order; only requesters count requests and syncs.  N = 1: every
+ *     request is a skip.
  * ---------------------------------------------------------------------- */
 enum {
   RIP_SCHED_TABLE = 0,      /* caller's periodic table (FIXED = one row)   */
@@ -115,7 +123,8 @@ enum {
   RIP_SCHED_GD = 3,         /* Global Division (+ slowdown filter)         */
   RIP_SCHED_SCRIPTED = 4,   /* Group Buffers fed by a caller's group list  */
   RIP_SCHED_RULE = 5,       /* the rule table of Fig. 9                    */
-  RIP_SCHED_INTER_INTRA = 6 /* Inter-Intra division (Sec. 5.2)             */
+  RIP_SCHED_INTER_INTRA = 6,/* Inter-Intra division (Sec. 5.2)             */
+  RIP_SCHED_ADPSGD = 7      /* AD-PSGD pairs with a passive partner (Fig. 3) */
 };
 
 typedef struct rip_sched rip_sched; /* opaque, library-owned */
@@ -123,7 +132,7 @@ typedef struct rip_sched rip_sched; /* opaque, library-owned */
 typedef struct rip_sched_cfg {
   int32_t n_workers;   /* N, 1..RIP_MAX_REPLICAS */
   int32_t mode;        /* RIP_SCHED_* */
-  uint64_t seed;       /* STATIC, RANDOM_GB, GD, INTER_INTRA */
+  uint64_t seed;       /* STATIC, RANDOM_GB, GD, INTER_INTRA, ADPSGD */
   int32_t group_size;  /* STATIC: N % group_size == 0, group_size >= 2 if N > 1 */
   int32_t period;      /* STATIC: rows per period (>= 1); TABLE: number of rows */
   int32_t kmin, kmax;  /* RANDOM_GB, GD, INTER_INTRA: 1 <= kmin <= kmax */
@@ -168,7 +177,7 @@ typedef struct rip_worker_state {
   int64_t syncs;     /* groups of this worker that ran */
   int64_t skips;     /* requests with no group (table modes) */
   int32_t waiting;   /* 1 if blocked in a P-Reduce */
-  int32_t gb_depth;  /* entries in its Group Buffer */
+  int32_t gb_depth;  /* entries in its Group Buffer (ADPSGD: 1 while its pair waits) */
 } rip_worker_state;
 
 /* Counters of one worker; requests == syncs + skips + waiting always. */

@@ -55,6 +55,7 @@ GD = 3
 SCRIPTED = 4
 RULE = 5
 INTER_INTRA = 6
+ADPSGD = 7
 
 SCHED_TAG = 3
 MAX_STATIC_ATTEMPTS = 1000
@@ -162,6 +163,10 @@ class Scheduler:
             if n != 4 * n_nodes:
                 raise ValueError("rule table needs n == 4 * n_nodes")
             self.rows = rule_table(n_nodes)
+        elif mode == ADPSGD:
+            self.rng = Stream(fold(seed, SCHED_TAG))
+            self.partner = [-1] * n
+            self.seq = [0] * n
         elif mode in (RANDOM_GB, GD, INTER_INTRA):
             if not 1 <= kmin <= kmax:
                 raise ValueError("need 1 <= kmin <= kmax")
@@ -261,6 +266,33 @@ class Scheduler:
             raise ValueError(f"scripted group {g} does not contain requester {i}")
         self._new_group(g)
 
+    # -- AD-PSGD (the baseline of Fig. 3) ------------------------------------
+    def _adpsgd_step(self, active):
+        """Each requester picks a random other worker j (Step 3 of Fig. 3)
+        and averages with it atomically (Step 4); j is passive and need not
+        be waiting.  Pairs whose workers are already locked this step wait;
+        the oldest request is served first."""
+        for i in active:
+            self.c[i] += 1
+            if self.n == 1:
+                self.skips[i] += 1
+                continue
+            x = self.rng.bounded(self.n - 1)
+            self.partner[i] = x if x < i else x + 1
+            self.seq[i] = self.next_id
+            self.next_id += 1
+            self.waiting[i] = True
+        locked, executed = set(), []
+        for i in sorted((w for w in range(self.n) if self.waiting[w]), key=lambda w: self.seq[w]):
+            j = self.partner[i]
+            if i in locked or j in locked:
+                continue
+            locked |= {i, j}
+            self.waiting[i] = False
+            self.syncs[i] += 1
+            executed.append(tuple(sorted((i, j))))
+        return executed
+
     # -- one request --------------------------------------------------------
     def _request(self, i: int):
         self.c[i] += 1
@@ -296,6 +328,8 @@ class Scheduler:
         n = self.n
         elig = [True] * n if eligible is None else [bool(e) for e in eligible]
         active = [i for i in range(n) if elig[i] and not self.waiting[i]]
+        if self.mode == ADPSGD:
+            return active, self._adpsgd_step(active)
         for i in active:
             self._request(i)
         ready = set()

@@ -34,6 +34,7 @@ SCHED_GD = 3
 SCHED_SCRIPTED = 4
 SCHED_RULE = 5
 SCHED_INTER_INTRA = 6
+SCHED_ADPSGD = 7
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
 

@@ -136,6 +136,8 @@ struct rip_sched {
     int64_t next_id = 0;
     Stream rng{0};
     size_t script_pos = 0;
+    std::vector<int32_t> partner;  // ADPSGD: chosen neighbour of a waiting requester
+    std::vector<int64_t> seq;      // ADPSGD: request order of a waiting requester
   } st;
   std::vector<Row> rows;       // table modes
   std::vector<Group> script;   // SCRIPTED
@@ -216,6 +218,45 @@ struct rip_sched {
     for (auto& [nd, ws] : rest)
       for (Group& g : chunks(ws)) new_group(std::move(g));
     for (auto& [nd, ws] : nodes) new_group(ws);
+  }
+
+  // AD-PSGD (Fig. 3): each requester picks a uniformly random other worker
+  // and averages with it atomically; the partner is passive.  Pairs whose
+  // workers are already locked in this step wait, oldest request first.
+  int32_t adpsgd_step(const int32_t* active, int32_t na, int32_t* group_offsets,
+                      int32_t* members, int32_t* n_groups) {
+    for (int32_t a = 0; a < na; ++a) {
+      const int i = active[a];
+      st.c[i] += 1;
+      if (n == 1) {
+        st.skips[i] += 1;
+        continue;
+      }
+      const int x = st.rng.bounded((uint32_t)(n - 1));
+      st.partner[i] = x < i ? x : x + 1;
+      st.seq[i] = st.next_id++;
+      st.waiting[i] = 1;
+    }
+    std::vector<int32_t> order;
+    for (int w = 0; w < n; ++w)
+      if (st.waiting[w]) order.push_back(w);
+    std::sort(order.begin(), order.end(),
+              [&](int32_t p, int32_t q) { return st.seq[p] < st.seq[q]; });
+    std::vector<uint8_t> locked(n, 0);
+    int32_t ng = 0, pos = 0;
+    group_offsets[0] = 0;
+    for (int32_t i : order) {
+      const int32_t j = st.partner[i];
+      if (locked[i] || locked[j]) continue;
+      locked[i] = locked[j] = 1;
+      st.waiting[i] = 0;
+      st.syncs[i] += 1;
+      members[pos++] = std::min(i, j);
+      members[pos++] = std::max(i, j);
+      group_offsets[++ng] = pos;
+    }
+    *n_groups = ng;
+    return RIP_OK;
   }
 
   int32_t request(int i) {
@@ -353,6 +394,12 @@ extern "C" int32_t rip_sched_create(const rip_sched_cfg* cfg, rip_sched** out) {
       s->st.rng.state = fold(cfg->seed, {(uint64_t)kSchedTag});
       break;
     }
+    case RIP_SCHED_ADPSGD: {
+      s->st.rng.state = fold(cfg->seed, {(uint64_t)kSchedTag});
+      s->st.partner.assign(n, -1);
+      s->st.seq.assign(n, 0);
+      break;
+    }
     case RIP_SCHED_SCRIPTED: {
       if (cfg->n_groups < 0 || (cfg->n_groups > 0 && (!cfg->group_offsets || !cfg->members))) {
         rc = rip::fail(RIP_E_INVAL, "SCRIPTED needs group_offsets and members");
@@ -399,6 +446,10 @@ extern "C" int32_t rip_schedule_groups(rip_sched* s, int64_t step, const uint8_t
   int32_t na = 0;
   for (int i = 0; i < n; ++i)
     if ((!eligible || eligible[i]) && !s->st.waiting[i]) active[na++] = i;
+  if (s->mode == RIP_SCHED_ADPSGD) {
+    *n_active = na;
+    return s->adpsgd_step(active, na, group_offsets, members, n_groups);
+  }
   for (int32_t a = 0; a < na; ++a) {
     int32_t rc = s->request(active[a]);
     if (rc != RIP_OK) {
@@ -447,6 +498,7 @@ extern "C" int32_t rip_sched_worker(const rip_sched* s, int32_t worker, rip_work
   out->syncs = s->st.syncs[worker];
   out->skips = s->st.skips[worker];
   out->waiting = s->st.waiting[worker];
-  out->gb_depth = (int32_t)s->st.gb[worker].size();
+  out->gb_depth = s->mode == RIP_SCHED_ADPSGD ? (int32_t)s->st.waiting[worker]
+                                              : (int32_t)s->st.gb[worker].size();
   return RIP_OK;
 }

@@ -34,7 +34,7 @@ VGG16_SEGMENTS = [1792, 36928, 73856, 147584, 295168, 590080, 590080, 1180160,
 RESNET50_PARAMS = 25_600_000
 
 # scheduler modes (values of the C ABI; the oracle uses the same numbers)
-TABLE, STATIC, RANDOM_GB, GD, SCRIPTED, RULE, INTER_INTRA = range(7)
+TABLE, STATIC, RANDOM_GB, GD, SCRIPTED, RULE, INTER_INTRA, ADPSGD = range(8)
 
 
 @dataclass

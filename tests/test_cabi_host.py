@@ -54,6 +54,9 @@ CASES = [
     (32, dict(mode=os_.GD, seed=9, kmin=3, kmax=3, c_thres=3),
      dict(mode=rip.SCHED_GD, seed=9, kmin=3, kmax=3, c_thres=3), 5),
     (16, dict(mode=os_.RULE, n_nodes=4), dict(mode=rip.SCHED_RULE, n_nodes=4), 3),
+    (32, dict(mode=os_.ADPSGD, seed=10), dict(mode=rip.SCHED_ADPSGD, seed=10), 4),
+    (5, dict(mode=os_.ADPSGD, seed=11), dict(mode=rip.SCHED_ADPSGD, seed=11), None),
+    (1, dict(mode=os_.ADPSGD, seed=12), dict(mode=rip.SCHED_ADPSGD, seed=12), None),
     (32, dict(mode=os_.INTER_INTRA, seed=6, kmin=2, kmax=4, n_nodes=4),
      dict(mode=rip.SCHED_INTER_INTRA, seed=6, kmin=2, kmax=4, n_nodes=4), 4),
     (24, dict(mode=os_.INTER_INTRA, seed=7, kmin=1, kmax=3, c_thres=2, n_nodes=3),
@@ -75,8 +78,9 @@ def test_scheduler_parity_with_oracle(n, okw, bkw, strag):
         assert rip.rip_schedule_groups(c, t, el) == o.step(t, el), f"step {t}"
     for i in range(n):
         ws = c.worker(i)
+        depth = int(o.waiting[i]) if o.mode == os_.ADPSGD else len(o.gb[i])
         assert (ws.requests, ws.syncs, ws.skips, bool(ws.waiting), ws.gb_depth) == \
-            (o.c[i], o.syncs[i], o.skips[i], o.waiting[i], len(o.gb[i]))
+            (o.c[i], o.syncs[i], o.skips[i], o.waiting[i], depth)
         assert ws.requests == ws.syncs + ws.skips + ws.waiting
 
 

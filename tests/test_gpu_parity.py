@@ -154,7 +154,8 @@ def test_random_gb_straggler_small():
 
 @pytest.mark.parametrize("mode,kw", [(wl.GD, dict(seed=6, kmin=2, kmax=4, c_thres=3)),
                                      (wl.RULE, dict(n_nodes=2)),
-                                     (wl.INTER_INTRA, dict(seed=8, kmin=2, kmax=3, n_nodes=2))])
+                                     (wl.INTER_INTRA, dict(seed=8, kmin=2, kmax=3, n_nodes=2)),
+                                     (wl.ADPSGD, dict(seed=9))])
 def test_other_schedulers_small(mode, kw):
     n = 8
     w = wl.scaled(wl.CONFIGS[4], [8193], steps=20, n=n, sched=dict(mode=mode, **kw))

@@ -248,6 +248,38 @@ def test_inter_intra_division(n, nodes, kmin, kmax):
     assert min(s.syncs) > 50
 
 
+def test_adpsgd_pairs():
+    """Fig. 3: every executed group is a pair holding its requester; pairs of
+    one step are disjoint; the partner is uniform over the other workers; the
+    oldest waiting request always runs (no starvation)."""
+    n = 8
+    s = os_.Scheduler(n, os_.ADPSGD, seed=13)
+    partner_counts = [[0] * n for _ in range(n)]
+    for t in range(3000):
+        elig = [True] * n
+        elig[0] = (t % 4 == 0)
+        waiting_before = {w for w in range(n) if s.waiting[w]}
+        act, groups = s.step(t, elig)
+        check_step_invariants(s, act, groups, n)
+        requesters = set(act) | waiting_before
+        oldest = min((w for w in requesters if w in act or w in waiting_before),
+                     key=lambda w: s.seq[w], default=None)
+        for g in groups:
+            assert len(g) == 2
+            assert g[0] in requesters or g[1] in requesters
+        if requesters:
+            assert any(oldest in g for g in groups)
+        for i in act:
+            if s.waiting[i] or any(i in g for g in groups):
+                partner_counts[i][s.partner[i]] += 1
+    for i in range(1, n):
+        row = [partner_counts[i][j] for j in range(n) if j != i]
+        assert partner_counts[i][i] == 0
+        assert max(row) < 1.4 * min(row)
+    one = os_.Scheduler(1, os_.ADPSGD, seed=1)
+    assert one.step(0) == ([0], []) and one.skips == [1]
+
+
 def test_inter_intra_rejects_uneven_nodes():
     with pytest.raises(ValueError):
         os_.Scheduler(10, os_.INTER_INTRA, kmin=2, kmax=2, n_nodes=4)
