@@ -34,6 +34,8 @@ METRIC = "P-Reduce+update effective HBM GB/s and % of MI355X HBM peak"
 KERNEL_SOURCES = ["paper_1909_08029_amd/csrc/rip_kernels.hip",
                   "paper_1909_08029_amd/csrc/rip_kernel_args.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+SCHEDULE_NAMES = ["table", "static", "random_gb", "global_division", "scripted", "rule",
+                  "inter_intra", "adpsgd"]
 
 
 def err(msg):
@@ -235,7 +237,7 @@ def main():
             "layout": args.layout,
             "storage": "bf16" if w.dtype == DTYPE_BF16 else "fp32",
             "optimizer": f"sgd lr={w.lr}" + (f" momentum={w.momentum}" if w.momentum else ""),
-            "schedule": w.sched.get("mode"),
+            "schedule": SCHEDULE_NAMES[w.sched["mode"]],
             "grad_ring": w.grad_ring,
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
             "host_schedule_us_per_step": round(sched_us, 2),

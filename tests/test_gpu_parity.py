@@ -288,8 +288,11 @@ def test_full_size_config_windows(cfg, steps, layout):
     osch = oracle_scheduler(w)
     assert run.schedule == [osch.step(t, w.eligible(t)) for t in range(steps)]
     bounds = np.cumsum(w.seg_numel)[:-1].tolist()
-    windows = sample_windows(w.numel, 12, 4096, seed=cfg, must=bounds)
+    windows = sample_windows(w.numel, 32, 1 << 16, seed=cfg, must=bounds)
+    covered = len(set().union(*(range(a, b) for a, b in windows))) if w.numel < 1 << 24 else \
+        sum(b - a for a, b in windows)
     worst = check_against_oracle(run, windows, f"config{cfg}")
-    log(f"config {cfg}: {len(windows)} windows x {w.n} replicas ok, max rel err {worst:.2e}")
+    log(f"config {cfg}: {len(windows)} windows of up to 65536 x {w.n} replicas ok "
+        f"({100.0 * covered / w.numel:.3f}% of each replica), max rel err {worst:.2e}")
     del run
     torch.cuda.empty_cache()
