@@ -112,6 +112,9 @@ def main():
     ap.add_argument("--grad-ring", type=int, default=None)
     ap.add_argument("--max-blocks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--unfused", action="store_true",
+                    help="ablation: rip_local_step then a pure rip_preduce per step "
+                         "(two passes over memory; reported with its own bytes)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM counters)")
     args = ap.parse_args()
@@ -165,13 +168,21 @@ def main():
         nonlocal t
         active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
         h = handles[w.grad_slot(t)]
+        opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
+                   nesterov=w.nesterov)
         if ev is not None:
             ev[0].record(stream)
-        rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, stream=stream,
-                        weight_decay=w.weight_decay, nesterov=w.nesterov)
+        if args.unfused:
+            if active:
+                rip.rip_local_step(h, active, w.lr, **opt)
+            rip.rip_preduce(h, groups, stream=stream)
+        else:
+            rip.rip_preduce(h, groups, active, lr=w.lr, **opt)
         if ev is not None:
             ev[1].record(stream)
         t += 1
+        if args.unfused:
+            return w.alg_bytes_unfused(active, groups)
         return w.alg_bytes(active, groups)
 
     for _ in range(args.warmup):
@@ -208,7 +219,7 @@ def main():
     mean_kernel_ms = sum(ms for _, ms in launched) / max(1, len(launched))
     achieved = mean_launch_bytes / (mean_kernel_ms * 1e-3) / 1e9 if launched else 0.0
     traffic = None
-    if args.layout == "flat" and not args.grad_ring:
+    if args.layout == "flat" and not args.grad_ring and not args.unfused:
         traffic = load_traffic(w.name, mean_launch_bytes)
 
     cpu = None
@@ -242,6 +253,7 @@ def main():
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
             "host_schedule_us_per_step": round(sched_us, 2),
             "parallelism": "single-gpu",
+            "pass": "unfused (local step, then P-Reduce)" if args.unfused else "fused",
         },
         "roofline": {
             "bound": "hbm",

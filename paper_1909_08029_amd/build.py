@@ -53,9 +53,22 @@ def build_seedgen(out: str = LIBSEEDGEN):
     os.replace(tmp, out)
 
 
+NATIVE_SMOKE = os.path.join(ROOT, "tests", "native", "cabi_smoke")
+
+
+def build_native_smoke(out: str = NATIVE_SMOKE):
+    """A plain C++ program that uses librip through include/rip.h only."""
+    tmp = out + ".tmp"
+    _run([HIPCC, f"--offload-arch={ARCH}", "-O2", "-std=c++17", "-Wall",
+          "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "tests", "native", "cabi_smoke.cpp"),
+          "-L", PKG, "-lrip", "-Wl,-rpath,$ORIGIN/../../paper_1909_08029_amd", "-o", tmp])
+    os.replace(tmp, out)
+
+
 def build_all():
     build_librip()
     build_seedgen()
+    build_native_smoke()
 
 
 if __name__ == "__main__":

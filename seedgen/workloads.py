@@ -88,6 +88,17 @@ class Workload:
         b -= sum(2 * s for g in groups if len(g) == 1 and g[0] not in act)
         return b * P
 
+    def alg_bytes_unfused(self, active: Sequence[int], groups: Sequence[Sequence[int]]) -> int:
+        """Minimum HBM bytes of the same step done as two passes: the local
+        update of every active replica (read w, g [, v], write w [, v]), then
+        a P-Reduce that reads and writes w of every member of a group of two
+        or more."""
+        s, P = self.esize, self.numel
+        per_active = 2 * s + s + (2 * s if self.momentum else 0)
+        b = per_active * len(set(active))
+        b += sum(2 * s * len(g) for g in groups if len(g) > 1)
+        return b * P
+
 
 CONFIGS: Dict[int, Workload] = {
     1: Workload("c1_n4_p1m_fp32_fixed", 4, [1_048_576], DTYPE_F32, 0.1, 0.0, 0.01,
