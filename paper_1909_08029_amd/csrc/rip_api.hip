@@ -41,6 +41,7 @@ void clear_error() { g_last_error.clear(); }
 struct rip_replicas {
   int32_t n = 0, n_seg = 0, dtype = 0, device = 0;
   int32_t lds_per_cu = 0;  // bytes of LDS per compute unit on `device`
+  int64_t numel0 = 0;      // elements of segment 0 (the whole range when flat)
   bool has_grad = false, has_mom = false;
   int64_t tiles[rip::kTileOptions] = {};  // tiles per unit, by slot option
   void* dmem = nullptr;  // ptab [3][S][N] u64 | seg_numel [S] i64 | seg_tile0 [4][S+1] i64
@@ -68,10 +69,11 @@ namespace {
 
 // Waves per CU at which the fused kernel sustained the most HBM bandwidth on
 // MI355X (measured over workgroup caps of 4-12 waves per CU): more resident
-// waves add outstanding requests without adding bandwidth.  bf16 storage
-// does more ALU work per byte and peaks with fewer waves; momentum moves five
-// streams per member and peaks slightly below plain SGD.
-int target_waves_per_cu(bool bf16, bool mom) { return bf16 ? 8 : (mom ? 9 : 10); }
+// waves add outstanding requests without adding bandwidth.  Tiles already
+// keep at least one 16-byte load per member stream in flight per lane, so
+// the wide units (momentum: three streams per member; bf16: eight elements
+// of ALU work per 16 bytes) peak with fewer waves than plain fp32 SGD.
+int target_waves_per_cu(bool bf16, bool mom) { return (bf16 || mom) ? 6 : 10; }
 
 int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
 int elem_size(int32_t dtype) { return dtype == RIP_BF16 ? 2 : 4; }
@@ -187,6 +189,7 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   h->has_grad = grad != nullptr;
   h->has_mom = mom != nullptr;
   for (int o = 0; o < rip::kTileOptions; ++o) h->tiles[o] = tile0[(size_t)o * (S + 1) + S];
+  h->numel0 = numel[0];
   hipError_t e = hipGetDevice(&h->device);
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&h->lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
@@ -304,6 +307,10 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
     a.unit_work0[u + 1] = (uint32_t)work;
   }
   a.work = (uint32_t)work;
+  a.uniform_tiles = units > 0 ? a.unit_work0[1] : 0;
+  for (int32_t u = 1; u < units && a.uniform_tiles; ++u)
+    if (a.unit_work0[u + 1] - a.unit_work0[u] != a.uniform_tiles) a.uniform_tiles = 0;
+  a.flat_numel = r->n_seg == 1 ? r->numel0 : 0;
   return RIP_OK;
 }
 

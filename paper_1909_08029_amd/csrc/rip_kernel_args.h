@@ -13,7 +13,7 @@ namespace rip {
 #define RIP_BLOCK 64
 #endif
 #ifndef RIP_LOADS_IN_FLIGHT
-#define RIP_LOADS_IN_FLIGHT 24
+#define RIP_LOADS_IN_FLIGHT 12
 #endif
 constexpr int kBlock = RIP_BLOCK;  // threads per workgroup: one wave64
 constexpr int kMaxK = 8;           // largest group size with a specialized path
@@ -42,11 +42,14 @@ struct StepArgs {
                               // segment, for tiles of 1, 2, 4, 8 slots
   int32_t n_seg, n_rep, n_units;
   uint32_t work;              // work items (tiles) of all units
+  uint32_t uniform_tiles;     // tiles per unit when all units have the same count, else 0
+  int64_t flat_numel;         // elements of the only segment when n_seg == 1
   float lr, mu, wd;
   int32_t nesterov;
   uint32_t unit_work0[RIP_MAX_REPLICAS + 1];  // first work item of each unit
-  uint16_t unit_off[RIP_MAX_REPLICAS + 1];    // unit u = member[unit_off[u] .. unit_off[u+1])
-  uint16_t member[RIP_MAX_REPLICAS];          // replica ids, ascending within a unit
+  // 16-bit tables start 4-byte aligned: the kernel reads them as dwords
+  alignas(4) uint16_t unit_off[RIP_MAX_REPLICAS + 1];  // unit u = member[unit_off[u] .. unit_off[u+1])
+  alignas(4) uint16_t member[RIP_MAX_REPLICAS];        // replica ids, ascending within a unit
   uint32_t active_bits[RIP_MAX_REPLICAS / 32];  // replicas doing their local update
 };
 

@@ -69,6 +69,24 @@ __device__ __forceinline__ void st16(char* p, u32x4 v) {
 #endif
 }
 
+// The launch tables (the kernel argument's arrays, the registered pointer and
+// segment tables) are never written while a launch runs.  Reading them
+// through the constant address space lets the compiler fetch these
+// wave-uniform values with scalar loads; read as ordinary global memory they
+// become vector loads that wait behind the streaming traffic (the kernel's
+// own stores could alias them, as far as the compiler can tell).
+#define RIP_CONST __attribute__((address_space(4)))
+
+template <typename T>
+__device__ __forceinline__ T cld(const T* p, int64_t i) {
+  return ((const RIP_CONST T*)p)[i];
+}
+// 16-bit entry i of a 4-byte-aligned table, read as its containing dword.
+__device__ __forceinline__ int cld16(const uint16_t* p, int i) {
+  const uint32_t word = ((const RIP_CONST uint32_t*)p)[i >> 1];
+  return (int)((i & 1) ? (word >> 16) : (word & 0xFFFFu));
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xFFFF0000u); }
 
@@ -185,17 +203,26 @@ struct Members {
   bool act[kMaxK];
 };
 
-template <int K>
+template <int K, bool MOM>
 __device__ __forceinline__ void load_members(const StepArgs& a, int base, int seg, Members& m) {
   const int plane = a.n_seg * a.n_rep;
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    const int id = a.member[base + j];
+    const int id = cld16(a.member, base + j);
     const int idx = seg * a.n_rep + id;
-    m.w[j] = reinterpret_cast<char*>(a.ptab[idx]);
-    m.g[j] = reinterpret_cast<const char*>(a.ptab[plane + idx]);
-    m.v[j] = reinterpret_cast<char*>(a.ptab[2 * plane + idx]);
-    m.act[j] = (a.active_bits[id >> 5] >> (id & 31)) & 1u;
+    m.w[j] = reinterpret_cast<char*>(cld(a.ptab, idx));
+    m.g[j] = reinterpret_cast<const char*>(cld(a.ptab, plane + idx));
+    m.v[j] = reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx));
+    m.act[j] = (cld(a.active_bits, id >> 5) >> (id & 31)) & 1u;
+  }
+  // Materialize every member's pointers and flag here, so one wait covers
+  // all of these scalar loads.  Left alone, the compiler sinks each pointer
+  // load next to its use, and every vector load then waits for its own
+  // scalar round trip: the wave's loads go out one at a time.
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    asm volatile("" ::"s"(m.w[j]), "s"(m.g[j]), "s"((int)m.act[j]));
+    if constexpr (MOM) asm volatile("" ::"s"(m.v[j]));
   }
 }
 
@@ -256,14 +283,14 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
   for (int64_t e = begin + threadIdx.x; e < end; e += kBlock) {
     float s = 0.0f;
     for (int j = 0; j < k; ++j) {
-      const int id = a.member[base + j];
+      const int id = cld16(a.member, base + j);
       const int idx = seg * a.n_rep + id;
-      char* w = reinterpret_cast<char*>(a.ptab[idx]);
+      char* w = reinterpret_cast<char*>(cld(a.ptab, idx));
       float x = ld1<BF16>(w, e);
-      if ((a.active_bits[id >> 5] >> (id & 31)) & 1u) {
-        const float g = ld1<BF16>(reinterpret_cast<const char*>(a.ptab[plane + idx]), e);
+      if ((cld(a.active_bits, id >> 5) >> (id & 31)) & 1u) {
+        const float g = ld1<BF16>(reinterpret_cast<const char*>(cld(a.ptab, plane + idx)), e);
         if constexpr (MOM) {
-          char* vp = reinterpret_cast<char*>(a.ptab[2 * plane + idx]);
+          char* vp = reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx));
           float v = ld1<BF16>(vp, e);
           x = update<true>(x, g, v, o);
           st1<BF16>(vp, e, v);
@@ -276,24 +303,10 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
     }
     if (k > 1) s = s * inv_k;
     for (int j = 0; j < k; ++j) {
-      const int id = a.member[base + j];
-      st1<BF16>(reinterpret_cast<char*>(a.ptab[seg * a.n_rep + id]), e, s);
+      const int id = cld16(a.member, base + j);
+      st1<BF16>(reinterpret_cast<char*>(cld(a.ptab, seg * a.n_rep + id)), e, s);
     }
   }
-}
-
-template <int K, bool BF16, bool MOM>
-__device__ __forceinline__ void full_tile(const StepArgs& a, int base, int seg, int64_t e_tile) {
-  constexpr int SL = 1 << slot_log2(K, MOM);
-  constexpr int N = Vec<BF16>::N;
-  constexpr int esize = BF16 ? 2 : 4;
-  Members m;
-  load_members<K>(a, base, seg, m);
-  int64_t off[SL];
-#pragma unroll
-  for (int u = 0; u < SL; ++u)
-    off[u] = (e_tile + (int64_t)(u * kBlock + (int)threadIdx.x) * N) * esize;
-  tile_slots<K, SL, BF16, MOM>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
 }
 
 // Last index i in [0, n) with v[i] <= x (v ascending, v[0] <= x).
@@ -302,39 +315,74 @@ __device__ __forceinline__ int last_le(const T* v, int n, X x) {
   int lo = 0, hi = n - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if ((X)v[mid] <= x) lo = mid; else hi = mid - 1;
+    if ((X)cld(v, mid) <= x) lo = mid; else hi = mid - 1;
   }
   return lo;
+}
+
+// One tile of a unit of K members (K <= kMaxK, or 0 for the element-wise path
+// with any k).  The tile geometry is a compile-time constant here, so a
+// workgroup reaches its first vector load after a handful of scalar
+// instructions: a flat handle needs no segment search at all.
+template <int K, bool BF16, bool MOM>
+__device__ __forceinline__ void unit_tile(const StepArgs& a, int base, int k, int64_t tile) {
+  constexpr int O = slot_log2(K == 0 ? kMaxK + 1 : K, MOM);
+  constexpr int SL = 1 << O;
+  constexpr int N = Vec<BF16>::N;
+  constexpr int64_t TE = (int64_t)kBlock * N * SL;  // elements per tile
+  int seg = 0;
+  int64_t e_tile, numel;
+  if (a.n_seg == 1) {
+    e_tile = tile * TE;
+    numel = a.flat_numel;
+  } else {
+    const int64_t* tile0 = a.seg_tile0 + O * (a.n_seg + 1);
+    seg = last_le(tile0, a.n_seg, tile);
+    e_tile = (tile - cld(tile0, seg)) * TE;
+    numel = cld(a.seg_numel, seg);
+  }
+  if constexpr (K > 0) {
+    if (e_tile + TE <= numel) {
+      constexpr int esize = BF16 ? 2 : 4;
+      Members m;
+      load_members<K, MOM>(a, base, seg, m);
+      int64_t off[SL];
+#pragma unroll
+      for (int u = 0; u < SL; ++u)
+        off[u] = (e_tile + (int64_t)(u * kBlock + (int)threadIdx.x) * N) * esize;
+      tile_slots<K, SL, BF16, MOM>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
+      return;
+    }
+  }
+  const int64_t end = (e_tile + TE < numel) ? e_tile + TE : numel;
+  elementwise<BF16, MOM>(a, base, k, seg, e_tile, end);
 }
 
 template <bool BF16, bool MOM>
 __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
   for (uint32_t w = blockIdx.x; w < a.work; w += gridDim.x) {
-    const int unit = last_le(a.unit_work0, a.n_units, w);
-    const int64_t tile = (int64_t)(w - a.unit_work0[unit]);
-    const int base = a.unit_off[unit];
-    const int k = a.unit_off[unit + 1] - base;
-    const int o = slot_log2(k, MOM);
-    const int64_t* tile0 = a.seg_tile0 + o * (a.n_seg + 1);
-    const int seg = last_le(tile0, a.n_seg, tile);
-    const int64_t tile_elems = ((int64_t)kBlock * Vec<BF16>::N) << o;
-    const int64_t e_tile = (tile - tile0[seg]) * tile_elems;
-    const int64_t numel = a.seg_numel[seg];
-    if (e_tile + tile_elems <= numel) {
-      switch (k) {
-        case 1: full_tile<1, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 2: full_tile<2, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 3: full_tile<3, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 4: full_tile<4, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 5: full_tile<5, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 6: full_tile<6, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 7: full_tile<7, BF16, MOM>(a, base, seg, e_tile); continue;
-        case 8: full_tile<8, BF16, MOM>(a, base, seg, e_tile); continue;
-        default: break;
-      }
+    int unit;
+    int64_t tile;
+    if (a.uniform_tiles) {  // every unit has the same tile count
+      unit = (int)(w / a.uniform_tiles);
+      tile = (int64_t)(w - (uint32_t)unit * a.uniform_tiles);
+    } else {
+      unit = last_le(a.unit_work0, a.n_units, w);
+      tile = (int64_t)(w - cld(a.unit_work0, unit));
     }
-    const int64_t end = (e_tile + tile_elems < numel) ? e_tile + tile_elems : numel;
-    elementwise<BF16, MOM>(a, base, k, seg, e_tile, end);
+    const int base = cld16(a.unit_off, unit);
+    const int k = cld16(a.unit_off, unit + 1) - base;
+    switch (k) {
+      case 1: unit_tile<1, BF16, MOM>(a, base, k, tile); break;
+      case 2: unit_tile<2, BF16, MOM>(a, base, k, tile); break;
+      case 3: unit_tile<3, BF16, MOM>(a, base, k, tile); break;
+      case 4: unit_tile<4, BF16, MOM>(a, base, k, tile); break;
+      case 5: unit_tile<5, BF16, MOM>(a, base, k, tile); break;
+      case 6: unit_tile<6, BF16, MOM>(a, base, k, tile); break;
+      case 7: unit_tile<7, BF16, MOM>(a, base, k, tile); break;
+      case 8: unit_tile<8, BF16, MOM>(a, base, k, tile); break;
+      default: unit_tile<0, BF16, MOM>(a, base, k, tile); break;
+    }
   }
 }
 
