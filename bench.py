@@ -23,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -117,6 +118,8 @@ def main():
                          "(two passes over memory; reported with its own bytes)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM counters)")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="only run the bare-stream HBM ceiling program (random vs zero data)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -125,6 +128,13 @@ def main():
               "MI355X's HBM and this build has no multi-GPU path; run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.ceiling:
+        exe = os.path.join(ROOT, "paper_1909_08029_amd", "stream_ceiling")
+        if not os.path.exists(exe):
+            err("stream_ceiling is not built; run __graft_entry__.build()")
+            sys.exit(1)
+        sys.exit(subprocess.run([exe]).returncode)
 
     import torch
     import paper_1909_08029_amd as rip

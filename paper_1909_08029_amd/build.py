@@ -65,10 +65,22 @@ def build_native_smoke(out: str = NATIVE_SMOKE):
     os.replace(tmp, out)
 
 
+STREAM_CEILING = os.path.join(PKG, "stream_ceiling")
+
+
+def build_stream_ceiling(out: str = STREAM_CEILING):
+    """The bare-stream HBM ceiling program run by `bench.py --ceiling`."""
+    tmp = out + ".tmp"
+    flags = [f for f in COMMON if f not in ("-fPIC", "-shared")]
+    _run([HIPCC, *flags, os.path.join(PKG, "csrc", "stream_ceiling.hip"), "-o", tmp])
+    os.replace(tmp, out)
+
+
 def build_all():
     build_librip()
     build_seedgen()
     build_native_smoke()
+    build_stream_ceiling()
 
 
 if __name__ == "__main__":
