@@ -9,6 +9,9 @@
 //   2R1W     w <- w - lr * g on one replica (the lone local update)
 //   group4   four replicas averaged after their update (8 reads, 4 writes),
 //            the shape of a P-Reduce group of four
+//   group8m  eight replicas with momentum averaged after their update
+//            (24 reads, 16 writes), the shape of a group of eight with
+//            momentum
 //
 // Every stream is 1 GiB.  The buffers are measured twice: filled with
 // random values (as the workloads are) and zero-filled, because the
@@ -33,7 +36,7 @@ __device__ __forceinline__ void store_nt(char* p, f32x4 v) {
 }
 
 constexpr int kLanes = 64;
-constexpr int kStreams = 8;
+constexpr int kStreams = 24;
 
 struct Streams {
   char* p[kStreams];
@@ -41,7 +44,7 @@ struct Streams {
   float lr;
 };
 
-enum Kind { kRead = 0, kCopy = 1, k2R1W = 2, kGroup4 = 3 };
+enum Kind { kRead = 0, kCopy = 1, k2R1W = 2, kGroup4 = 3, kGroup8Mom = 4 };
 
 template <int KIND>
 __global__ __launch_bounds__(kLanes) void stream_kernel(Streams s) {
@@ -64,6 +67,24 @@ __global__ __launch_bounds__(kLanes) void stream_kernel(Streams s) {
     } else if constexpr (KIND == k2R1W) {
       const f32x4 w = load_nt(s.p[0] + off), g = load_nt(s.p[1] + off);
       store_nt(s.p[0] + off, w - s.lr * g);
+    } else if constexpr (KIND == kGroup8Mom) {
+      f32x4 w[8], g[8], v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        w[j] = load_nt(s.p[j] + off);
+        g[j] = load_nt(s.p[8 + j] + off);
+        v[j] = load_nt(s.p[16 + j] + off);
+      }
+      f32x4 sum = {0, 0, 0, 0};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[j] = 0.9f * v[j] + g[j];
+        store_nt(s.p[16 + j] + off, v[j]);
+        sum = sum + (w[j] - s.lr * v[j]);
+      }
+      sum = sum * 0.125f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) store_nt(s.p[j] + off, sum);
     } else {
       f32x4 w[4], g[4];
 #pragma unroll
@@ -147,7 +168,10 @@ int main() {
   for (int random = 1; random >= 0; --random) {
     for (int j = 0; j < kStreams; ++j) {
       if (random) {
-        // weights ~U[-1,1), gradients ~U[-0.01,0.01)
+        // p[0..3] ~U[-1,1) and every other stream ~U[-0.01,0.01): random
+        // mantissas and signs everywhere (group4 reads weights p[0..3] and
+        // gradients p[4..7]; group8m weights p[0..7], gradients p[8..15],
+        // momenta p[16..23])
         hipLaunchKernelGGL(fill_random, dim3(8192), dim3(256), 0, 0, reinterpret_cast<float*>(s.p[j]),
                            bytes / 4, (uint64_t)(1000 + j), j < 4 ? 1.0f : 0.01f);
       } else if (hipMemset(s.p[j], 0, bytes) != hipSuccess) {
@@ -155,16 +179,19 @@ int main() {
       }
     }
     if (hipDeviceSynchronize() != hipSuccess) return 1;
-    for (int waves : {6, 8, 10, 12, 16, 0}) {
+    for (int waves : {4, 5, 6, 8, 10, 12, 16, 0}) {
       const size_t lds = waves ? ((size_t)(lds_per_cu / waves) & ~(size_t)255) : 0;
       const double t_read = time_ms<kRead>(s, lds), t_copy = time_ms<kCopy>(s, lds);
       const double t_2r1w = time_ms<k2R1W>(s, lds), t_g4 = time_ms<kGroup4>(s, lds);
-      if (t_read < 0 || t_copy < 0 || t_2r1w < 0 || t_g4 < 0) return 1;
+      const double t_g8m = time_ms<kGroup8Mom>(s, lds);
+      if (t_read < 0 || t_copy < 0 || t_2r1w < 0 || t_g4 < 0 || t_g8m < 0) return 1;
       char cap[16];
       std::snprintf(cap, sizeof cap, "%d", waves);
-      std::printf("data=%-6s waves/CU=%-4s read %7.1f  copy %7.1f  2R1W %7.1f  group4 %7.1f GB/s\n",
+      std::printf("data=%-6s waves/CU=%-4s read %7.1f  copy %7.1f  2R1W %7.1f  group4 %7.1f  "
+                  "group8m %7.1f GB/s\n",
                   random ? "random" : "zero", waves ? cap : "max", gb / t_read * 1e3,
-                  2 * gb / t_copy * 1e3, 3 * gb / t_2r1w * 1e3, 12 * gb / t_g4 * 1e3);
+                  2 * gb / t_copy * 1e3, 3 * gb / t_2r1w * 1e3, 12 * gb / t_g4 * 1e3,
+                  40 * gb / t_g8m * 1e3);
       std::fflush(stdout);
     }
   }
