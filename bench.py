@@ -69,6 +69,24 @@ def load_traffic(workload: str, alg_bytes_per_launch: float):
     return int(round(ent["traffic_over_alg"] * alg_bytes_per_launch))
 
 
+def host_cpu() -> str:
+    """CPU model, logical CPUs and the CPUs this process may run on."""
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        allowed = os.cpu_count()
+    return f"{model}, {os.cpu_count()} logical CPUs, {allowed} in this process's affinity"
+
+
 def cpu_baseline(w, seconds: float = 12.0):
     """The oracle as it stands, single-threaded numpy, on one window of every
     replica, for as many steps of the workload's schedule as fit the budget
@@ -100,7 +118,7 @@ def cpu_baseline(w, seconds: float = 12.0):
     return dict(value=round(nbytes / spent / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
                 sample=f"{steps} steps of the workload schedule on elements [0, {width}) of all "
                        f"{w.n} replicas ({100.0 * width / w.numel:.1f}% of each replica), "
-                       f"numpy single-threaded, host has {os.cpu_count()} CPUs; "
+                       f"numpy single-threaded on {host_cpu()}; "
                        f"{spent:.1f} s timed, update+average only")
 
 
@@ -228,6 +246,7 @@ def main():
     value = total_bytes / wall / 1e9
     mean_launch_bytes = sum(b for b, _ in launched) / max(1, len(launched))
     mean_kernel_ms = sum(ms for _, ms in launched) / max(1, len(launched))
+    median_kernel_ms = sorted(ms for _, ms in launched)[len(launched) // 2] if launched else 0.0
     achieved = mean_launch_bytes / (mean_kernel_ms * 1e-3) / 1e9 if launched else 0.0
     traffic = None
     if args.layout == "flat" and not args.grad_ring and not args.unfused:
@@ -275,6 +294,8 @@ def main():
             "traffic": traffic,
             "alg_bytes_per_launch": int(mean_launch_bytes),
             "mean_kernel_us": round(mean_kernel_ms * 1e3, 2),
+            "median_kernel_us": round(median_kernel_ms * 1e3, 2),
+            "launches_timed": len(launched),
         },
         "cpu_baseline": cpu,
     }

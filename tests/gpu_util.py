@@ -24,9 +24,25 @@ def to_f32(x: np.ndarray, dtype: int) -> np.ndarray:
     return x
 
 
+def max_ulp(gpu: np.ndarray, ora: np.ndarray, dtype: int) -> int:
+    """Largest distance in units in the last place between matching elements
+    (bit patterns mapped to a monotone integer order; +0 and -0 are 0 apart)."""
+    if gpu.size == 0:
+        return 0
+    if dtype == DTYPE_BF16:
+        bg, bo, sign = gpu.view(np.uint16).astype(np.int64), ora.view(np.uint16).astype(np.int64), 1 << 15
+    else:
+        bg, bo, sign = gpu.view(np.uint32).astype(np.int64), ora.view(np.uint32).astype(np.int64), 1 << 31
+
+    def order(b):
+        return np.where(b >= sign, sign - b, b)
+    return int(np.abs(order(bg) - order(bo)).max())
+
+
 def compare(gpu: np.ndarray, ora: np.ndarray, dtype: int, what: str = ""):
     """Returns (max relative error, bit mismatches); asserts the tolerance and
-    bit-exactness (the kernels follow the oracle's operation order)."""
+    bit-exactness (the kernels follow the oracle's operation order).  Failure
+    messages also give the largest ulp distance."""
     assert gpu.shape == ora.shape, (gpu.shape, ora.shape)
     g, o = to_f32(gpu, dtype).astype(np.float64), to_f32(ora, dtype).astype(np.float64)
     denom = np.maximum(np.abs(o), 2.0 ** -126)
@@ -36,8 +52,11 @@ def compare(gpu: np.ndarray, ora: np.ndarray, dtype: int, what: str = ""):
     bits_g = gpu.view(np.uint16 if dtype == DTYPE_BF16 else np.uint32)
     bits_o = ora.view(np.uint16 if dtype == DTYPE_BF16 else np.uint32)
     mism = int(np.count_nonzero(bits_g != bits_o))
-    assert max_rel <= TOL[dtype], f"{what}: max rel err {max_rel:.3e} > {TOL[dtype]}"
-    assert mism == 0, f"{what}: {mism} bit mismatches (max rel err {max_rel:.3e})"
+    if max_rel > TOL[dtype] or mism:
+        ulp = max_ulp(gpu, ora, dtype)
+        assert max_rel <= TOL[dtype], \
+            f"{what}: max rel err {max_rel:.3e} > {TOL[dtype]} ({mism} bit mismatches, max {ulp} ulp)"
+        assert mism == 0, f"{what}: {mism} bit mismatches (max rel err {max_rel:.3e}, max {ulp} ulp)"
     return max_rel, mism
 
 
