@@ -144,7 +144,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: every replica of the P-Reduce path lives in one "
-              "MI355X's HBM and this build has no multi-GPU path; run with --gpus 1.",
+              "MI355X's HBM and this library has no multi-GPU path; run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
