@@ -131,6 +131,8 @@ def main():
     ap.add_argument("--layout", default="flat", choices=["flat", "separate"])
     ap.add_argument("--grad-ring", type=int, default=None)
     ap.add_argument("--max-blocks", type=int, default=0)
+    ap.add_argument("--blocks-per-cu", type=int, default=0,
+                    help="resident workgroups per CU (0 = the library's per-shape default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--unfused", action="store_true",
                     help="ablation: rip_local_step then a pure rip_preduce per step "
@@ -181,6 +183,8 @@ def main():
     err(f"[bench] workload {w.name}: N={w.n} P={w.numel} layout={args.layout}")
     if args.max_blocks:
         rip.rip_set_max_blocks(args.max_blocks)
+    if args.blocks_per_cu:
+        rip.rip_set_blocks_per_cu(args.blocks_per_cu)
 
     st = wl.DeviceState(w, args.layout)
     st.fill()

@@ -71,13 +71,16 @@ extern "C" int32_t rip_set_max_blocks(int32_t max_blocks) {
 namespace {
 
 // Waves per CU at which the fused kernel sustained the most HBM bandwidth on
-// MI355X (measured over workgroup caps of 5-16 waves per CU): more resident
+// MI355X (measured over workgroup caps of 2-16 waves per CU): more resident
 // waves add outstanding requests without adding bandwidth.  With momentum a
-// lane already keeps three 16-byte loads per member in flight, so those
-// units peak with fewer waves; fp32 and bf16 plain SGD peak at 10.
+// lane already keeps three 16-byte loads per member in flight (24 for a group
+// of eight), so those units peak with fewer waves (group of eight: 4 waves
+// 6.09 TB/s, 6 waves 5.99); fp32 and bf16 plain SGD peak at 10.  Odd caps
+// measured the same as the even cap below them (the LDS reservation appears
+// to be granted per half of a CU's LDS), so only even caps are used.
 int target_waves_per_cu(bool bf16, bool mom) {
   (void)bf16;
-  return mom ? 6 : 10;
+  return mom ? 4 : 10;
 }
 
 int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
@@ -277,20 +280,31 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
 
   std::memset(&a, 0, sizeof a);
   int32_t units = 0, pos = 0;
-  a.unit_off[0] = 0;
+  std::vector<int32_t> unit_off(1, 0);
   for (int32_t g = 0; g < n_groups; ++g) {
     const int32_t b = group_offsets[g], e = group_offsets[g + 1];
     if (e - b == 1 && !is_active[members[b]]) continue;  // identity: nothing to do
-    for (int32_t j = b; j < e; ++j) a.member[pos++] = (uint16_t)members[j];
-    a.unit_off[++units] = (uint16_t)pos;
+    for (int32_t j = b; j < e; ++j) a.member[pos++] = (uint8_t)members[j];
+    unit_off.push_back(pos);
+    ++units;
   }
   for (int32_t id = 0; id < N; ++id)
     if (is_active[id] && !in_group[id]) {
-      a.member[pos++] = (uint16_t)id;
-      a.unit_off[++units] = (uint16_t)pos;
+      a.member[pos++] = (uint8_t)id;
+      unit_off.push_back(pos);
+      ++units;
     }
   for (int32_t id = 0; id < N; ++id)
     if (is_active[id]) a.active_bits[id >> 5] |= 1u << (id & 31);
+  for (int32_t u = 0; u < units; ++u) {
+    const int32_t b = unit_off[u], k = unit_off[u + 1] - b;
+    uint32_t act8 = 0;
+    for (int32_t j = 0; j < k && j < 8; ++j) act8 |= (uint32_t)is_active[a.member[b + j]] << j;
+    a.unit_info[u] = rip::unit_info_pack((uint32_t)b, (uint32_t)k, act8);
+  }
+  a.uniform_k = units > 0 ? (uint32_t)(unit_off[1] - unit_off[0]) : 0;
+  for (int32_t u = 1; u < units && a.uniform_k; ++u)
+    if ((uint32_t)(unit_off[u + 1] - unit_off[u]) != a.uniform_k) a.uniform_k = 0;
   a.ptab = r->d_ptab;
   a.seg_numel = r->d_numel;
   a.seg_tile0 = r->d_tile0;
@@ -305,7 +319,7 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
   int64_t work = 0;
   a.unit_work0[0] = 0;
   for (int32_t u = 0; u < units; ++u) {
-    const int k = a.unit_off[u + 1] - a.unit_off[u];
+    const int k = unit_off[u + 1] - unit_off[u];
     work += r->tiles[rip::slot_log2(k, mom)];
     if (work >= (int64_t)1 << 31)
       return rip::fail(RIP_E_UNSUPPORTED, "more than 2^31 tiles in one step (replicas too large)");
@@ -343,7 +357,8 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   if (bpc == 0) bpc = target_waves_per_cu(r->dtype == RIP_BF16, mom) * 64 / rip::kBlock;
   size_t lds = 0;
   if (bpc > 0 && r->lds_per_cu > 0) lds = (size_t)(r->lds_per_cu / bpc) & ~(size_t)255;
-  e = rip::launch_fused_step(a, r->dtype == RIP_BF16, mom, blocks, lds,
+  const bool ext = a.wd != 0.0f || a.nesterov != 0;
+  e = rip::launch_fused_step(a, r->dtype == RIP_BF16, mom, ext, blocks, lds,
                              static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return rip::fail(RIP_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   return RIP_OK;

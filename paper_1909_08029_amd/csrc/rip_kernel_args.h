@@ -33,7 +33,7 @@ constexpr int slot_log2(int k, bool mom) {
   return l;
 }
 
-// Passed by value as the kernel argument (about 2.2 KiB), so each launch
+// Passed by value as the kernel argument (about 2.4 KiB), so each launch
 // carries its own schedule and no device staging buffer is needed.
 struct StepArgs {
   const uint64_t* ptab;       // device [3][S][N]: param, grad, mom pointers
@@ -43,17 +43,33 @@ struct StepArgs {
   int32_t n_seg, n_rep, n_units;
   uint32_t work;              // work items (tiles) of all units
   uint32_t uniform_tiles;     // tiles per unit when all units have the same count, else 0
+  uint32_t uniform_k;         // members per unit when all units have the same size, else 0
   int64_t flat_numel;         // elements of the only segment when n_seg == 1
   float lr, mu, wd;
   int32_t nesterov;
   uint32_t unit_work0[RIP_MAX_REPLICAS + 1];  // first work item of each unit
-  // 16-bit tables start 4-byte aligned: the kernel reads them as dwords
-  alignas(4) uint16_t unit_off[RIP_MAX_REPLICAS + 1];  // unit u = member[unit_off[u] .. unit_off[u+1])
-  alignas(4) uint16_t member[RIP_MAX_REPLICAS];        // replica ids, ascending within a unit
+  uint32_t unit_info[RIP_MAX_REPLICAS];       // see unit_info_pack
+  // Replica ids, ascending within a unit; unit u = member[base_u .. base_u + k_u).
+  // The kernel reads the 16 bytes from the dword holding member[base_u], so
+  // the table is padded to keep that read inside it.
+  alignas(16) uint8_t member[RIP_MAX_REPLICAS + 16];
   uint32_t active_bits[RIP_MAX_REPLICAS / 32];  // replicas doing their local update
 };
 
-hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, int blocks,
+// One dword per unit: first member index (8 bits), member count k (9 bits),
+// and the update flags of its first eight members (bit j = member j is
+// active), so a workgroup learns its unit from a single scalar load.
+constexpr uint32_t unit_info_pack(uint32_t base, uint32_t k, uint32_t act8) {
+  return base | (k << 8) | (act8 << 17);
+}
+constexpr uint32_t unit_info_base(uint32_t info) { return info & 0xFFu; }
+constexpr uint32_t unit_info_k(uint32_t info) { return (info >> 8) & 0x1FFu; }
+constexpr uint32_t unit_info_act8(uint32_t info) { return info >> 17; }
+static_assert(RIP_MAX_REPLICAS <= 256, "unit_info packs member indices into 8 bits");
+
+// ext: weight decay or Nesterov momentum is on (the kernel variant that
+// handles them; the plain variant leaves them out of the arithmetic).
+hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, bool ext, int blocks,
                              size_t lds_bytes, hipStream_t stream);
 
 }  // namespace rip

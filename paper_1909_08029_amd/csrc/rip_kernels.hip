@@ -81,10 +81,26 @@ template <typename T>
 __device__ __forceinline__ T cld(const T* p, int64_t i) {
   return ((const RIP_CONST T*)p)[i];
 }
-// 16-bit entry i of a 4-byte-aligned table, read as its containing dword.
-__device__ __forceinline__ int cld16(const uint16_t* p, int i) {
-  const uint32_t word = ((const RIP_CONST uint32_t*)p)[i >> 1];
-  return (int)((i & 1) ? (word >> 16) : (word & 0xFFFFu));
+// Byte i of a 4-byte-aligned table, read as its containing dword.
+__device__ __forceinline__ int cld8(const uint8_t* p, int i) {
+  const uint32_t word = ((const RIP_CONST uint32_t*)p)[i >> 2];
+  return (int)((word >> ((i & 3) * 8)) & 0xFFu);
+}
+// Bytes i .. i+7 of the (16-byte aligned, padded) member table as one 64-bit
+// value, byte j in bits 8j..8j+7: one 16-byte scalar load of the aligned
+// dwords that hold them, then a funnel shift.
+typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint64_t cld8x8(const uint8_t* p, int i) {
+  const u32x4c d = ((const RIP_CONST u32x4c*)p)[i >> 4];
+  const u32x4c e = ((const RIP_CONST u32x4c*)p)[(i >> 4) + 1];
+  // 32 bytes d|e hold bytes (i & ~15) .. (i & ~15) + 31, which cover i .. i+7
+  const int sh = (i & 15) * 8;  // 0..120
+  const uint64_t q0 = d.x | ((uint64_t)d.y << 32), q1 = d.z | ((uint64_t)d.w << 32);
+  const uint64_t q2 = e.x | ((uint64_t)e.y << 32);
+  if (sh == 0) return q0;
+  if (sh < 64) return (q0 >> sh) | (q1 << (64 - sh));
+  if (sh == 64) return q1;
+  return (q1 >> (sh - 64)) | (q2 << (128 - sh));
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
@@ -179,18 +195,26 @@ __constant__ InvTable kInv = make_inv_table();
 //   g' = g + wd*w                       (only when weight decay is on)
 //   SGD:       u = w - lr*g'
 //   momentum:  v = mu*v + g';  u = w - lr*v,  or with Nesterov u = w - lr*(g' + mu*v)
-// wd and nesterov are wave-uniform, so their tests are scalar branches.
+// EXT selects the kernel variant that handles weight decay and Nesterov.
+// Their flags are wave-uniform, but the compiler turns the tests into
+// per-element selects, computing both sides: that more than doubles the
+// arithmetic per element, which costs bandwidth when few waves share a CU.
+// Plain SGD and heavy-ball momentum therefore get a variant without them;
+// with wd == 0 and no Nesterov both variants compute the same values.
 struct Opt {
   float lr, mu, wd;
   bool nesterov;
 };
 
-template <bool MOM>
+template <bool MOM, bool EXT>
 __device__ __forceinline__ float update(float w, float g, float& v, const Opt& o) {
-  if (o.wd != 0.0f) g = g + o.wd * w;
+  if constexpr (EXT) {
+    if (o.wd != 0.0f) g = g + o.wd * w;
+  }
   if constexpr (MOM) {
     v = o.mu * v + g;
-    return w - o.lr * (o.nesterov ? g + o.mu * v : v);
+    if constexpr (EXT) return w - o.lr * (o.nesterov ? g + o.mu * v : v);
+    return w - o.lr * v;
   } else {
     return w - o.lr * g;
   }
@@ -203,17 +227,20 @@ struct Members {
   bool act[kMaxK];
 };
 
+// The unit's member ids (one per byte of `ids`) came with the unit; their
+// pointers are 3K independent scalar loads, all issued before one wait.
 template <int K, bool MOM>
-__device__ __forceinline__ void load_members(const StepArgs& a, int base, int seg, Members& m) {
+__device__ __forceinline__ void load_members(const StepArgs& a, uint64_t ids, uint32_t act8,
+                                             int seg, Members& m) {
   const int plane = a.n_seg * a.n_rep;
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    const int id = cld16(a.member, base + j);
+    const int id = (int)((ids >> (8 * j)) & 0xFFu);
     const int idx = seg * a.n_rep + id;
     m.w[j] = reinterpret_cast<char*>(cld(a.ptab, idx));
     m.g[j] = reinterpret_cast<const char*>(cld(a.ptab, plane + idx));
     m.v[j] = reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx));
-    m.act[j] = (cld(a.active_bits, id >> 5) >> (id & 31)) & 1u;
+    m.act[j] = (act8 >> j) & 1u;
   }
   // Materialize every member's pointers and flag here, so one wait covers
   // all of these scalar loads.  Left alone, the compiler sinks each pointer
@@ -227,7 +254,7 @@ __device__ __forceinline__ void load_members(const StepArgs& a, int base, int se
 }
 
 // U consecutive 16-byte slots of a full tile for a unit of K members.
-template <int K, int U, bool BF16, bool MOM>
+template <int K, int U, bool BF16, bool MOM, bool EXT>
 __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off)[U],
                                            const Opt& o) {
   using V = Vec<BF16>;
@@ -244,6 +271,14 @@ __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off
         if constexpr (MOM) vv[u][j] = ld16(m.v[j] + off[u]);
       }
     }
+  // All arithmetic comes before the first store.  Stores count against the
+  // same vmcnt as loads, and because the gradient and momentum loads are
+  // conditional (active members only) the compiler's waits before each
+  // member's arithmetic are conservative: a momentum store issued between two
+  // members would make the next wait cover that store's completion, a full
+  // write round trip.  (A straight-line variant for groups whose members all
+  // update, with exact waits, measured no faster and slowed bf16 by 2%.)
+  u32x4 out[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     float s[N];
@@ -256,8 +291,8 @@ __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off
         V::unpack(gv[u][j], g);
         if constexpr (MOM) V::unpack(vv[u][j], v);
 #pragma unroll
-        for (int i = 0; i < N; ++i) x[i] = update<MOM>(x[i], g[i], v[i], o);
-        if constexpr (MOM) st16(m.v[j] + off[u], V::pack(v));
+        for (int i = 0; i < N; ++i) x[i] = update<MOM, EXT>(x[i], g[i], v[i], o);
+        if constexpr (MOM) vv[u][j] = V::pack(v);
       }
 #pragma unroll
       for (int i = 0; i < N; ++i) s[i] = (j == 0) ? x[i] : s[i] + x[i];
@@ -266,15 +301,26 @@ __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off
 #pragma unroll
       for (int i = 0; i < N; ++i) s[i] = s[i] * inv_k;
     }
-    const u32x4 out = V::pack(s);
-#pragma unroll
-    for (int j = 0; j < K; ++j) st16(m.w[j] + off[u], out);
+    out[u] = V::pack(s);
   }
+  // Keep the instruction scheduler from sinking arithmetic below the stores.
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (MOM) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < K; ++j)
+        if (m.act[j]) st16(m.v[j] + off[u], vv[u][j]);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int j = 0; j < K; ++j) st16(m.w[j] + off[u], out[u]);
 }
 
 // Element-wise path for a partial tile or any k: each thread walks elements
 // e0 + i*stride below `end`.
-template <bool BF16, bool MOM>
+template <bool BF16, bool MOM, bool EXT>
 __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t begin,
                             int64_t end) {
   const int plane = a.n_seg * a.n_rep;
@@ -283,7 +329,7 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
   for (int64_t e = begin + threadIdx.x; e < end; e += kBlock) {
     float s = 0.0f;
     for (int j = 0; j < k; ++j) {
-      const int id = cld16(a.member, base + j);
+      const int id = cld8(a.member, base + j);
       const int idx = seg * a.n_rep + id;
       char* w = reinterpret_cast<char*>(cld(a.ptab, idx));
       float x = ld1<BF16>(w, e);
@@ -292,18 +338,18 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
         if constexpr (MOM) {
           char* vp = reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx));
           float v = ld1<BF16>(vp, e);
-          x = update<true>(x, g, v, o);
+          x = update<true, EXT>(x, g, v, o);
           st1<BF16>(vp, e, v);
         } else {
           float unused = 0.0f;
-          x = update<false>(x, g, unused, o);
+          x = update<false, EXT>(x, g, unused, o);
         }
       }
       s = (j == 0) ? x : s + x;
     }
     if (k > 1) s = s * inv_k;
     for (int j = 0; j < k; ++j) {
-      const int id = cld16(a.member, base + j);
+      const int id = cld8(a.member, base + j);
       st1<BF16>(reinterpret_cast<char*>(cld(a.ptab, seg * a.n_rep + id)), e, s);
     }
   }
@@ -320,24 +366,39 @@ __device__ __forceinline__ int last_le(const T* v, int n, X x) {
   return lo;
 }
 
+// The unit a workgroup works on, as the main loop decoded it.
+struct Unit {
+  int base, k;    // member[base .. base + k)
+  uint32_t act8;  // update flags of members 0..7
+  uint64_t ids;   // member ids 0..7, one per byte
+};
+
+// Launch-wide values, read once per workgroup before anything else.
+struct Header {
+  uint32_t work, uniform_tiles, uniform_k;
+  int n_seg;
+  int64_t flat_numel;
+};
+
 // One tile of a unit of K members (K <= kMaxK, or 0 for the element-wise path
 // with any k).  The tile geometry is a compile-time constant here, so a
 // workgroup reaches its first vector load after a handful of scalar
 // instructions: a flat handle needs no segment search at all.
-template <int K, bool BF16, bool MOM>
-__device__ __forceinline__ void unit_tile(const StepArgs& a, int base, int k, int64_t tile) {
+template <int K, bool BF16, bool MOM, bool EXT>
+__device__ __forceinline__ void unit_tile(const StepArgs& a, const Header& h, const Unit& u,
+                                          int64_t tile) {
   constexpr int O = slot_log2(K == 0 ? kMaxK + 1 : K, MOM);
   constexpr int SL = 1 << O;
   constexpr int N = Vec<BF16>::N;
   constexpr int64_t TE = (int64_t)kBlock * N * SL;  // elements per tile
   int seg = 0;
   int64_t e_tile, numel;
-  if (a.n_seg == 1) {
+  if (h.n_seg == 1) {
     e_tile = tile * TE;
-    numel = a.flat_numel;
+    numel = h.flat_numel;
   } else {
-    const int64_t* tile0 = a.seg_tile0 + O * (a.n_seg + 1);
-    seg = last_le(tile0, a.n_seg, tile);
+    const int64_t* tile0 = a.seg_tile0 + O * (h.n_seg + 1);
+    seg = last_le(tile0, h.n_seg, tile);
     e_tile = (tile - cld(tile0, seg)) * TE;
     numel = cld(a.seg_numel, seg);
   }
@@ -345,55 +406,82 @@ __device__ __forceinline__ void unit_tile(const StepArgs& a, int base, int k, in
     if (e_tile + TE <= numel) {
       constexpr int esize = BF16 ? 2 : 4;
       Members m;
-      load_members<K, MOM>(a, base, seg, m);
+      load_members<K, MOM>(a, u.ids, u.act8, seg, m);
       int64_t off[SL];
 #pragma unroll
-      for (int u = 0; u < SL; ++u)
-        off[u] = (e_tile + (int64_t)(u * kBlock + (int)threadIdx.x) * N) * esize;
-      tile_slots<K, SL, BF16, MOM>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
+      for (int s = 0; s < SL; ++s)
+        off[s] = (e_tile + (int64_t)(s * kBlock + (int)threadIdx.x) * N) * esize;
+      tile_slots<K, SL, BF16, MOM, EXT>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
       return;
     }
   }
   const int64_t end = (e_tile + TE < numel) ? e_tile + TE : numel;
-  elementwise<BF16, MOM>(a, base, k, seg, e_tile, end);
+  elementwise<BF16, MOM, EXT>(a, u.base, u.k, seg, e_tile, end);
 }
 
-template <bool BF16, bool MOM>
+template <bool BF16, bool MOM, bool EXT>
 __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
-  for (uint32_t w = blockIdx.x; w < a.work; w += gridDim.x) {
+  // Load the whole header into scalar registers in one batch up front: left
+  // to itself the compiler spreads it over several batches (and loads
+  // flat_numel late, through a select of addresses), and every extra batch is
+  // one more dependent scalar round trip before the workgroup's first vector
+  // load.
+  const Header h{a.work, a.uniform_tiles, a.uniform_k, a.n_seg, a.flat_numel};
+  asm volatile("" ::"s"(h.work), "s"(h.uniform_tiles), "s"(h.uniform_k), "s"(h.n_seg),
+               "s"(h.flat_numel), "s"(a.ptab), "s"(a.n_rep), "s"(a.lr), "s"(a.mu), "s"(a.wd),
+               "s"(a.nesterov), "s"(a.n_units), "s"(a.seg_numel), "s"(a.seg_tile0));
+  for (uint32_t w = blockIdx.x; w < h.work; w += gridDim.x) {
     int unit;
     int64_t tile;
-    if (a.uniform_tiles) {  // every unit has the same tile count
-      unit = (int)(w / a.uniform_tiles);
-      tile = (int64_t)(w - (uint32_t)unit * a.uniform_tiles);
+    if (h.uniform_tiles) {  // every unit has the same tile count
+      unit = (int)(w / h.uniform_tiles);
+      tile = (int64_t)(w - (uint32_t)unit * h.uniform_tiles);
     } else {
       unit = last_le(a.unit_work0, a.n_units, w);
       tile = (int64_t)(w - cld(a.unit_work0, unit));
     }
-    const int base = cld16(a.unit_off, unit);
-    const int k = cld16(a.unit_off, unit + 1) - base;
-    switch (k) {
-      case 1: unit_tile<1, BF16, MOM>(a, base, k, tile); break;
-      case 2: unit_tile<2, BF16, MOM>(a, base, k, tile); break;
-      case 3: unit_tile<3, BF16, MOM>(a, base, k, tile); break;
-      case 4: unit_tile<4, BF16, MOM>(a, base, k, tile); break;
-      case 5: unit_tile<5, BF16, MOM>(a, base, k, tile); break;
-      case 6: unit_tile<6, BF16, MOM>(a, base, k, tile); break;
-      case 7: unit_tile<7, BF16, MOM>(a, base, k, tile); break;
-      case 8: unit_tile<8, BF16, MOM>(a, base, k, tile); break;
-      default: unit_tile<0, BF16, MOM>(a, base, k, tile); break;
+    // With equal-sized units the member window's address needs no load, so
+    // it is fetched together with the unit's info word: the unit costs one
+    // scalar round trip, its members' pointers a second.
+    const uint32_t info = cld(a.unit_info, unit);
+    Unit u;
+    if (h.uniform_k) {
+      u.k = (int)h.uniform_k;
+      u.base = unit * u.k;
+    } else {
+      u.k = (int)unit_info_k(info);
+      u.base = (int)unit_info_base(info);
+    }
+    u.act8 = unit_info_act8(info);
+    u.ids = cld8x8(a.member, u.base);
+    switch (u.k) {
+      case 1: unit_tile<1, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 2: unit_tile<2, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 3: unit_tile<3, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 4: unit_tile<4, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 5: unit_tile<5, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 6: unit_tile<6, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 7: unit_tile<7, BF16, MOM, EXT>(a, h, u, tile); break;
+      case 8: unit_tile<8, BF16, MOM, EXT>(a, h, u, tile); break;
+      default: unit_tile<0, BF16, MOM, EXT>(a, h, u, tile); break;
     }
   }
 }
 
 }  // namespace
 
-hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, int blocks,
+namespace {
+template <bool BF16, bool MOM>
+const void* kernel_for(bool ext) {
+  return ext ? reinterpret_cast<const void*>(&fused_step_kernel<BF16, MOM, true>)
+             : reinterpret_cast<const void*>(&fused_step_kernel<BF16, MOM, false>);
+}
+}  // namespace
+
+hipError_t launch_fused_step(const StepArgs& a, bool bf16, bool mom, bool ext, int blocks,
                              size_t lds_bytes, hipStream_t stream) {
-  const void* fn = bf16 ? (mom ? reinterpret_cast<const void*>(&fused_step_kernel<true, true>)
-                               : reinterpret_cast<const void*>(&fused_step_kernel<true, false>))
-                        : (mom ? reinterpret_cast<const void*>(&fused_step_kernel<false, true>)
-                               : reinterpret_cast<const void*>(&fused_step_kernel<false, false>));
+  const void* fn = bf16 ? (mom ? kernel_for<true, true>(ext) : kernel_for<true, false>(ext))
+                        : (mom ? kernel_for<false, true>(ext) : kernel_for<false, false>(ext));
   void* args[] = {const_cast<StepArgs*>(&a)};
   // hipLaunchKernel reports this launch's own status (not an earlier sticky error).
   // lds_bytes is a reservation only (the kernel uses no LDS): it caps how
