@@ -45,10 +45,17 @@ def err(msg):
 
 
 def kernel_hash() -> str:
+    """First 16 hex digits of sha256 over the kernel and launch sources with
+    comments and whitespace removed, so an edit to a comment does not
+    orphan counters taken on the same code."""
+    import re
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -141,6 +148,8 @@ def main():
                     help="only run a plain device copy of known size (to scale HBM counters)")
     ap.add_argument("--ceiling", action="store_true",
                     help="only run the bare-stream HBM ceiling program (random vs zero data)")
+    ap.add_argument("--ceiling-xcd", action="store_true",
+                    help="only run the ceiling program's XCD tile-placement sweep")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -150,12 +159,12 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    if args.ceiling:
+    if args.ceiling or args.ceiling_xcd:
         exe = os.path.join(ROOT, "paper_1909_08029_amd", "stream_ceiling")
         if not os.path.exists(exe):
             err("stream_ceiling is not built; run __graft_entry__.build()")
             sys.exit(1)
-        sys.exit(subprocess.run([exe]).returncode)
+        sys.exit(subprocess.run([exe] + (["xcd"] if args.ceiling_xcd else [])).returncode)
 
     import torch
     import paper_1909_08029_amd as rip

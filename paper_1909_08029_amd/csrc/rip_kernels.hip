@@ -9,10 +9,11 @@
 // members' buffers, so the launch is a list of (unit, tile) work items, one
 // per single-wave workgroup, unit after unit.  A tile is 64 lanes x 1-8
 // slots x 16 bytes of each member stream; the slot count shrinks as the
-// unit's number of streams grows (see slot_log2), so every wave keeps about
-// 24 16-byte loads in flight per lane whatever the group size.  The host caps
-// residency at 8-10 waves per CU (an LDS reservation): HBM3E delivered its
-// best rate at that depth of outstanding requests, not at full occupancy.
+// unit's number of streams grows (see slot_log2), so every lane keeps about
+// 12 16-byte loads in flight whatever the group size (24 for a group of eight
+// with momentum).  The host caps residency at 10 waves per CU, 4 with
+// momentum (an LDS reservation): HBM3E delivered its best rate at that depth
+// of outstanding requests, not at full occupancy.
 // A workgroup handles one unit, so the unit's size k, its member ids and their active
 // flags are wave-uniform: they sit in scalar registers and every branch on
 // them is a scalar branch.  Each thread issues the loads of all members
