@@ -26,6 +26,13 @@
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Device
  *    work is asynchronous on that stream.
  *  - Handles are not thread-safe; use one handle per thread or lock.
+ *  - Graph capture: rip_local_step and rip_preduce enqueue exactly one
+ *    kernel launch (or nothing, when the step has no work), with the whole
+ *    step -- schedule, optimizer scalars, the handle's pointer table -- in
+ *    the kernel argument, and no memset, copy or allocation.  They may be
+ *    called on a stream under HIP graph capture; each replay re-applies the
+ *    captured step to whatever the buffers hold then.  The replicas handle
+ *    must outlive the graph.
  */
 #ifndef RIP_H
 #define RIP_H
