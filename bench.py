@@ -137,6 +137,9 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--layout", default="flat", choices=["flat", "separate"])
     ap.add_argument("--grad-ring", type=int, default=None)
+    ap.add_argument("--schedule", default=None,
+                    help="replace the workload's schedule by one of the paper's policies: "
+                         "random_gb, gd, gd_filter, inter_intra, static, adpsgd, allreduce")
     ap.add_argument("--max-blocks", type=int, default=0)
     ap.add_argument("--blocks-per-cu", type=int, default=0,
                     help="resident workgroups per CU (0 = the library's per-shape default)")
@@ -189,6 +192,8 @@ def main():
     w = wl.CONFIGS[args.config]
     if args.grad_ring:
         w = wl.scaled(w, w.seg_numel, grad_ring=args.grad_ring)
+    if args.schedule:
+        w = wl.with_schedule(w, args.schedule)
     err(f"[bench] workload {w.name}: N={w.n} P={w.numel} layout={args.layout}")
     if args.max_blocks:
         rip.rip_set_max_blocks(args.max_blocks)
@@ -206,9 +211,17 @@ def main():
     stream = torch.cuda.current_stream()
     t = 0
 
+    stats = dict(steps=0, updates=0, groups=0, members=0, empty=0)
+
     def one_step(ev=None):
         nonlocal t
         active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
+        if ev is not None:
+            stats["steps"] += 1
+            stats["updates"] += len(active)
+            stats["groups"] += sum(1 for g in groups if len(g) > 1)
+            stats["members"] += sum(len(g) for g in groups if len(g) > 1)
+            stats["empty"] += 0 if (active or any(len(g) > 1 for g in groups)) else 1
         h = handles[w.grad_slot(t)]
         opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
                    nesterov=w.nesterov)
@@ -291,7 +304,14 @@ def main():
             "layout": args.layout,
             "storage": "bf16" if w.dtype == DTYPE_BF16 else "fp32",
             "optimizer": f"sgd lr={w.lr}" + (f" momentum={w.momentum}" if w.momentum else ""),
-            "schedule": SCHEDULE_NAMES[w.sched["mode"]],
+            "schedule": args.schedule or SCHEDULE_NAMES[w.sched["mode"]],
+            "schedule_stats": {
+                "local_updates_per_step": round(stats["updates"] / max(1, stats["steps"]), 3),
+                "groups_per_step": round(stats["groups"] / max(1, stats["steps"]), 3),
+                "mean_group_size": round(stats["members"] / max(1, stats["groups"]), 3),
+                "steps_without_work": stats["empty"],
+                "local_updates_per_s": round(stats["updates"] / wall, 1),
+            },
             "grad_ring": w.grad_ring,
             "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
             "host_schedule_us_per_step": round(sched_us, 2),

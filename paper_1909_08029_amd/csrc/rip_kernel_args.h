@@ -24,7 +24,7 @@ constexpr int kTileOptions = 4;    // tiles of 1, 2, 4 or 8 slots per thread
 // loads outstanding per thread (k members x w, g and, with momentum, v), so
 // small groups and lone updates still have enough bytes in flight while a
 // workgroup moves a similar number of bytes whatever the group size.  Groups
-// above kMaxK take the element-wise path with one slot.
+// above kMaxK use one slot and stream their members in chunks of kMaxK.
 constexpr int slot_log2(int k, bool mom) {
   if (k > kMaxK) return 0;
   const int s = RIP_LOADS_IN_FLIGHT / (k * (mom ? 3 : 2));

@@ -319,7 +319,7 @@ __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off
     for (int j = 0; j < K; ++j) st16(m.w[j] + off[u], out[u]);
 }
 
-// Element-wise path for a partial tile or any k: each thread walks elements
+// Element-wise path for a partial tile (any k): each thread walks elements
 // e0 + i*stride below `end`.
 template <bool BF16, bool MOM, bool EXT>
 __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t begin,
@@ -353,6 +353,98 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
       const int id = cld8(a.member, base + j);
       st1<BF16>(reinterpret_cast<char*>(cld(a.ptab, seg * a.n_rep + id)), e, s);
     }
+  }
+}
+
+// A full tile of a group larger than kMaxK (All-Reduce as one group of every
+// worker, large divisions): the members stream through in chunks of eight,
+// 16-byte accesses as in tile_slots, their updated values summed into one
+// running fp32 sum in ascending member order; the mean then goes to every
+// member.  Each member's w, g and v are read once and written once, as in
+// the specialized paths; only the member pointers are fetched twice.
+template <bool BF16, bool MOM, bool EXT>
+__device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, int seg,
+                                          int64_t e_tile) {
+  using V = Vec<BF16>;
+  constexpr int N = V::N;
+  constexpr int C = kMaxK;  // members per chunk
+  const int plane = a.n_seg * a.n_rep;
+  const Opt o{a.lr, a.mu, a.wd, a.nesterov != 0};
+  const int64_t off = (e_tile + (int64_t)threadIdx.x * N) * (BF16 ? 2 : 4);
+  float s[N];
+  for (int j0 = 0; j0 < k; j0 += C) {
+    const uint64_t ids = cld8x8(a.member, base + j0);  // bytes past the unit are unused
+    char* w[C];
+    const char* g[C];
+    char* v[C];
+    bool act[C];
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) {
+      const int id = (int)((ids >> (8 * jj)) & 0xFFu);
+      const int idx = seg * a.n_rep + id;
+      const bool in = j0 + jj < k;
+      w[jj] = in ? reinterpret_cast<char*>(cld(a.ptab, idx)) : nullptr;
+      g[jj] = in ? reinterpret_cast<const char*>(cld(a.ptab, plane + idx)) : nullptr;
+      v[jj] = in && MOM ? reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx)) : nullptr;
+      act[jj] = in && ((cld(a.active_bits, id >> 5) >> (id & 31)) & 1u);
+    }
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) {
+      asm volatile("" ::"s"(w[jj]), "s"(g[jj]), "s"((int)act[jj]));
+      if constexpr (MOM) asm volatile("" ::"s"(v[jj]));
+    }
+    u32x4 wv[C], gv[C], vv[C];
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) {
+      if (j0 + jj < k) {
+        wv[jj] = ld16(w[jj] + off);
+        if (act[jj]) {
+          gv[jj] = ld16(g[jj] + off);
+          if constexpr (MOM) vv[jj] = ld16(v[jj] + off);
+        }
+      }
+    }
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) {
+      if (j0 + jj < k) {
+        float x[N];
+        V::unpack(wv[jj], x);
+        if (act[jj]) {
+          float gf[N], vf[N];
+          V::unpack(gv[jj], gf);
+          if constexpr (MOM) V::unpack(vv[jj], vf);
+#pragma unroll
+          for (int i = 0; i < N; ++i) x[i] = update<MOM, EXT>(x[i], gf[i], vf[i], o);
+          if constexpr (MOM) vv[jj] = V::pack(vf);
+        }
+#pragma unroll
+        for (int i = 0; i < N; ++i) s[i] = (j0 + jj == 0) ? x[i] : s[i] + x[i];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (MOM) {
+#pragma unroll
+      for (int jj = 0; jj < C; ++jj)
+        if (act[jj]) st16(v[jj] + off, vv[jj]);
+    }
+  }
+  const float inv_k = kInv.v[k];
+#pragma unroll
+  for (int i = 0; i < N; ++i) s[i] = s[i] * inv_k;
+  const u32x4 out = V::pack(s);
+  for (int j0 = 0; j0 < k; j0 += C) {
+    const uint64_t ids = cld8x8(a.member, base + j0);
+    char* w[C];
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) {
+      const int id = (int)((ids >> (8 * jj)) & 0xFFu);
+      w[jj] = j0 + jj < k ? reinterpret_cast<char*>(cld(a.ptab, seg * a.n_rep + id)) : nullptr;
+    }
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) asm volatile("" ::"s"(w[jj]));
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj)
+      if (j0 + jj < k) st16(w[jj] + off, out);
   }
 }
 
@@ -413,6 +505,11 @@ __device__ __forceinline__ void unit_tile(const StepArgs& a, const Header& h, co
       for (int s = 0; s < SL; ++s)
         off[s] = (e_tile + (int64_t)(s * kBlock + (int)threadIdx.x) * N) * esize;
       tile_slots<K, SL, BF16, MOM, EXT>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
+      return;
+    }
+  } else {
+    if (e_tile + TE <= numel) {
+      wide_tile<BF16, MOM, EXT>(a, u.base, u.k, seg, e_tile);
       return;
     }
   }

@@ -116,6 +116,36 @@ CONFIGS: Dict[int, Workload] = {
 }
 
 
+# The scheduling policies the paper compares, as schedules of the same fused
+# kernel on a workload's replicas: random groups with Group Buffers (Step 3 of
+# Fig. 4), Global Division with and without the slowdown filter (Sec. 5.1,
+# Sec. 5.3), Inter-Intra synchronization with 4 workers per node (Sec. 5.2),
+# a seeded static schedule of groups of 4 (Sec. 4.2), AD-PSGD's random pairs
+# (Fig. 3) and All-Reduce as one group of every worker.  Group sizes 2..8
+# follow the heterogeneous workload; the filter threshold C_thres (a tunable
+# constant in the paper) is 4, the straggler's update interval.
+SCHEDULE_VARIANTS = ("random_gb", "gd", "gd_filter", "inter_intra", "static", "adpsgd",
+                     "allreduce")
+
+
+def with_schedule(w: Workload, name: str) -> Workload:
+    """The workload with its schedule replaced by one of SCHEDULE_VARIANTS."""
+    n, seed = w.n, w.seed
+    sched = {
+        "random_gb": dict(mode=RANDOM_GB, seed=seed, kmin=2, kmax=8),
+        "gd": dict(mode=GD, seed=seed, kmin=2, kmax=8),
+        "gd_filter": dict(mode=GD, seed=seed, kmin=2, kmax=8, c_thres=4),
+        "inter_intra": dict(mode=INTER_INTRA, seed=seed, kmin=2, kmax=8, c_thres=4,
+                            n_nodes=max(1, n // 4)),
+        "static": dict(mode=STATIC, seed=seed, group_size=4 if n % 4 == 0 else 1, period=4),
+        "adpsgd": dict(mode=ADPSGD, seed=seed),
+        "allreduce": dict(mode=TABLE, table=[[tuple(range(n))]]),
+    }
+    if name not in sched:
+        raise ValueError(f"unknown schedule {name!r}; choose from {SCHEDULE_VARIANTS}")
+    return scaled(w, w.seg_numel, sched=sched[name], name=f"{w.name}_{name}")
+
+
 def scaled(w: Workload, numel: Sequence[int], **kw) -> Workload:
     """Same recipe with other segment sizes (for small parity cases)."""
     d = dict(w.__dict__)

@@ -82,6 +82,28 @@ def test_every_group_size_small(dtype, P):
 
 
 @pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+@pytest.mark.parametrize("wd,nesterov,mom", [(0.0, False, 0.9), (1e-2, True, 0.9),
+                                             (5e-3, False, 0.0)])
+def test_large_groups_with_optimizers(dtype, wd, nesterov, mom):
+    """Groups above the specialized sizes (9, 16 and 23 members: one, two and
+    three chunks of eight, a ragged last chunk) with momentum, weight decay
+    and Nesterov, some members not updating, over segments with ragged tails."""
+    table = [[tuple(range(0, 9)), tuple(range(9, 25)), tuple(range(25, 48))],
+             [tuple(range(1, 48, 2)), tuple(range(0, 48, 2))]]
+    w = wl.Workload("wide", 48, [3 * 4096 + 11, 2048, 9], dtype,
+                    0.1 if dtype == DTYPE_F32 else 20.0, mom, 0.01,
+                    dict(mode=wl.TABLE, table=table), 6, 23, straggler_every=3,
+                    param_sigma=1.0 if dtype == DTYPE_F32 else 0.05, grad_ring=3,
+                    weight_decay=wd, nesterov=nesterov)
+    for layout in ("flat", "separate"):
+        log(f"case wide groups dtype={dtype} wd={wd} nesterov={nesterov} mom={mom} {layout}")
+        run = GpuRun(w, layout)
+        run.run(w.steps)
+        assert any(len(g) > 8 for _, gs in run.schedule for g in gs)
+        check_against_oracle(run, full_windows(w.numel), f"wide {layout}")
+
+
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
 @pytest.mark.parametrize("layout", ["flat", "separate"])
 def test_segments_with_momentum(dtype, layout):
     """Layer-sized segments (the first VGG-16 tensors, a ragged one, an empty
@@ -294,5 +316,27 @@ def test_full_size_config_windows(cfg, steps, layout):
     worst = check_against_oracle(run, windows, f"config{cfg}")
     log(f"config {cfg}: {len(windows)} windows of up to 65536 x {w.n} replicas ok "
         f"({100.0 * covered / w.numel:.3f}% of each replica), max rel err {worst:.2e}")
+    del run
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# the paper's scheduling policies on the heterogeneous workload's full shape
+# (N = 32 fp32 replicas of 25.6M, worker 0 at a quarter of the others' rate)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", [n for n in wl.SCHEDULE_VARIANTS if n != "random_gb"])
+def test_full_size_schedule_variants(name):
+    import torch
+    w = wl.with_schedule(wl.CONFIGS[4], name)
+    steps = 12
+    log(f"case full config 4 schedule={name} steps={steps}")
+    run = GpuRun(w)
+    run.run(steps)
+    torch.cuda.synchronize()
+    osch = oracle_scheduler(w)
+    assert run.schedule == [osch.step(t, w.eligible(t)) for t in range(steps)]
+    windows = sample_windows(w.numel, 8, 1 << 15, seed=40)
+    worst = check_against_oracle(run, windows, f"config4 {name}")
+    log(f"config 4 {name}: {len(windows)} windows x {w.n} replicas ok, max rel err {worst:.2e}")
     del run
     torch.cuda.empty_cache()
