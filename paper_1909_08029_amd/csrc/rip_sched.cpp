@@ -348,7 +348,8 @@ extern "C" int32_t rip_sched_create(const rip_sched_cfg* cfg, rip_sched** out) {
           if (rc != RIP_OK) break;
           s->rows[r].push_back(std::move(grp));
         }
-        if (rc == RIP_OK) sort_row(s->rows[r]);
+        // The caller's order within a row is kept: groups of a step come out
+        // by (iteration, position in the row as given).
       }
       // A period without any group is a table of pure local steps.
       if (rc == RIP_OK && cfg->n_groups == 0) s->rows.assign(cfg->period, Row{});

@@ -65,6 +65,9 @@ CASES = [
      dict(mode=rip.SCHED_RANDOM_GB, seed=2 ** 64 - 1, kmin=1, kmax=9), 2),
     (12, dict(mode=os_.TABLE, table=[[(0, 5), (1, 2, 3)], [], [(4, 6, 7, 8, 9, 10, 11)]]),
      dict(mode=rip.SCHED_TABLE, table=[[(0, 5), (1, 2, 3)], [], [(4, 6, 7, 8, 9, 10, 11)]]), 3),
+    # rows not ordered by first member, singletons: output keeps the row's own order
+    (10, dict(mode=os_.TABLE, table=[[(3, 9), (0, 7), (5,)], [(6, 8), (4,), (1, 2, 5)]]),
+     dict(mode=rip.SCHED_TABLE, table=[[(3, 9), (0, 7), (5,)], [(6, 8), (4,), (1, 2, 5)]]), 3),
 ]
 
 
