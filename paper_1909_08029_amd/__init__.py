@@ -158,6 +158,7 @@ class Scheduler:
         h = ctypes.c_void_p()
         _check(lib.rip_sched_create(ctypes.byref(cfg), ctypes.byref(h)))
         self._h = h
+        self._destroy = lib.rip_sched_destroy  # still reachable at interpreter exit
         n = n_workers
         self._act = (ctypes.c_int32 * n)()
         self._off = (ctypes.c_int32 * (n + 1))()
@@ -167,7 +168,7 @@ class Scheduler:
 
     def close(self):
         if getattr(self, "_h", None):
-            lib.rip_sched_destroy(self._h)
+            self._destroy(self._h)
             self._h = None
 
     __del__ = close
@@ -241,10 +242,11 @@ class Replicas:
                                        self._keep[0], self._keep[1], self._keep[2],
                                        ctypes.byref(h)))
         self._h = h
+        self._destroy = lib.rip_replicas_destroy  # still reachable at interpreter exit
 
     def close(self):
         if getattr(self, "_h", None):
-            lib.rip_replicas_destroy(self._h)
+            self._destroy(self._h)
             self._h = None
 
     __del__ = close
