@@ -203,6 +203,39 @@ def test_allreduce_and_max_replicas():
         rip.Scheduler(257, wl.TABLE, table=[[(0,)]])
 
 
+@pytest.mark.parametrize("dtype,P", [(DTYPE_F32, 1_100_000_007), (DTYPE_BF16, 2_200_000_011)])
+def test_buffers_beyond_4gib(dtype, P):
+    """Replica buffers of 4.4 GB: byte offsets past 2^32 in the tiled paths
+    and the ragged tail; windows straddle the 4 GiB offset and the end."""
+    import torch
+    w = wl.Workload("big", 3, [P], dtype, 0.1 if dtype == DTYPE_F32 else 20.0, 0.0, 0.01,
+                    dict(mode=wl.TABLE, table=[[(0, 1)], [(1, 2)]]), 2, 81, grad_ring=1,
+                    param_sigma=1.0 if dtype == DTYPE_F32 else 0.05)
+    log(f"case buffers beyond 4 GiB dtype={dtype} P={P}")
+    run = GpuRun(w)
+    run.run(w.steps)
+    torch.cuda.synchronize()
+    boundary = (1 << 32) // w.esize
+    windows = sample_windows(P, 8, 1 << 15, seed=82, must=[boundary])
+    assert any(a < boundary < b for a, b in windows) and windows[-1][1] == P
+    check_against_oracle(run, windows, f"beyond 4 GiB dtype={dtype}")
+    del run
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+def test_single_replica(dtype):
+    """N = 1: the local update alone (its own group of one), with momentum."""
+    w = wl.Workload("one", 1, [3 * 4096 + 7], dtype, 0.1 if dtype == DTYPE_F32 else 20.0, 0.9,
+                    0.01, dict(mode=wl.TABLE, table=[[(0,)], []]), 4, 83, grad_ring=2,
+                    param_sigma=1.0 if dtype == DTYPE_F32 else 0.05)
+    log(f"case single replica dtype={dtype}")
+    run = GpuRun(w)
+    run.run(w.steps)
+    assert [a for a, _ in run.schedule] == [[0]] * 4
+    check_against_oracle(run, full_windows(w.numel), "N=1")
+
+
 def test_pure_preduce_invariants_and_untouched():
     """Members end bit-identical, replicas outside every group keep their
     bytes, and the replica sum is preserved (doubly stochastic F^G)."""
