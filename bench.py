@@ -189,7 +189,7 @@ def main():
         print(json.dumps({"calibration": "copy", "bytes_read_per_launch": 4 * n,
                           "bytes_written_per_launch": 4 * n, "launches": 5}), flush=True)
         return
-    w = wl.CONFIGS[args.config]
+    w = wl.WORKLOADS[args.config]
     if args.grad_ring:
         w = wl.scaled(w, w.seg_numel, grad_ring=args.grad_ring)
     if args.schedule:

@@ -100,7 +100,7 @@ class Workload:
         return b * P
 
 
-CONFIGS: Dict[int, Workload] = {
+WORKLOADS: Dict[int, Workload] = {
     1: Workload("c1_n4_p1m_fp32_fixed", 4, [1_048_576], DTYPE_F32, 0.1, 0.0, 0.01,
                 dict(mode=TABLE, table=[[(0, 1, 2)]]), 10, 1,
                 note="fits the 256 MB Infinity Cache: not an HBM measurement"),

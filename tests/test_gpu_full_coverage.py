@@ -59,7 +59,7 @@ def _oracle_chunk(w: wl.Workload, schedule, p, grads, v, got_p, got_v, label):
 @pytest.mark.parametrize("cfg,steps", CASES)
 def test_full_coverage(cfg, steps):
     import torch
-    w = wl.CONFIGS[cfg]
+    w = wl.WORKLOADS[cfg]
     log(f"case full coverage config {cfg} ({w.name}) steps={steps}")
     t0 = time.time()
     run = GpuRun(w, "flat")

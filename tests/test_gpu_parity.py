@@ -48,7 +48,7 @@ def test_seedgen_gpu_matches_cpu():
 
 def test_config1_full_trajectory():
     """N=4 fp32 replicas of 1,048,576; SGD lr 0.1; group {0,1,2}; 10 steps."""
-    w = wl.CONFIGS[1]
+    w = wl.WORKLOADS[1]
     log(f"case {w.name}")
     run = GpuRun(w)
     run.run(w.steps)
@@ -109,7 +109,7 @@ def test_segments_with_momentum(dtype, layout):
     """Layer-sized segments (the first VGG-16 tensors, a ragged one, an empty
     one), momentum 0.9, static groups of 8 over 16 replicas."""
     segs = [1792, 36928, 7, 0, 73856 + 3, 5000]
-    w = wl.scaled(wl.CONFIGS[3], segs, steps=5, grad_ring=3,
+    w = wl.scaled(wl.WORKLOADS[3], segs, steps=5, grad_ring=3,
                   dtype=dtype, lr=0.1 if dtype == DTYPE_F32 else 20.0)
     log(f"case segments layout={layout} dtype={dtype}")
     run = GpuRun(w, layout)
@@ -121,7 +121,7 @@ def test_segments_with_momentum(dtype, layout):
 def test_unfused_local_step_then_preduce(dtype):
     """rip_local_step followed by a pure rip_preduce: two stores (for bf16,
     two roundings), as the oracle's unfused form."""
-    w = wl.scaled(wl.CONFIGS[4], [40_000 + 9], steps=12, n=12, dtype=dtype,
+    w = wl.scaled(wl.WORKLOADS[4], [40_000 + 9], steps=12, n=12, dtype=dtype,
                   lr=0.1 if dtype == DTYPE_F32 else 30.0, momentum=0.9,
                   sched=dict(mode=wl.RANDOM_GB, seed=8, kmin=2, kmax=5))
     log(f"case unfused dtype={dtype}")
@@ -142,7 +142,7 @@ def test_optimizer_variants(dtype, wd, nesterov, mom, fused):
     """Weight decay and Nesterov momentum, fused and unfused, on random
     groups with a straggler (so groups also hold members that did not
     update this step)."""
-    w = wl.scaled(wl.CONFIGS[3], [3 * 4096 + 11, 777], steps=8, n=8, dtype=dtype,
+    w = wl.scaled(wl.WORKLOADS[3], [3 * 4096 + 11, 777], steps=8, n=8, dtype=dtype,
                   lr=0.1 if dtype == DTYPE_F32 else 20.0, momentum=mom, weight_decay=wd,
                   nesterov=nesterov, sched=dict(mode=wl.RANDOM_GB, seed=9, kmin=2, kmax=8),
                   straggler_every=3, grad_ring=3)
@@ -165,7 +165,7 @@ def test_nesterov_without_momentum_is_rejected():
 
 
 def test_random_gb_straggler_small():
-    w = wl.scaled(wl.CONFIGS[4], [3 * 4096 + 17], steps=40)
+    w = wl.scaled(wl.WORKLOADS[4], [3 * 4096 + 17], steps=40)
     log("case random-gb small")
     run = GpuRun(w)
     run.run(w.steps)
@@ -180,7 +180,7 @@ def test_random_gb_straggler_small():
                                      (wl.ADPSGD, dict(seed=9))])
 def test_other_schedulers_small(mode, kw):
     n = 8
-    w = wl.scaled(wl.CONFIGS[4], [8193], steps=20, n=n, sched=dict(mode=mode, **kw))
+    w = wl.scaled(wl.WORKLOADS[4], [8193], steps=20, n=n, sched=dict(mode=mode, **kw))
     log(f"case scheduler mode={mode}")
     run = GpuRun(w)
     run.run(w.steps)
@@ -335,7 +335,7 @@ FULL = [(2, 6, "flat"), (3, 4, "flat"), (3, 3, "separate"), (4, 24, "flat"), (5,
 @pytest.mark.parametrize("cfg,steps,layout", FULL)
 def test_full_size_config_windows(cfg, steps, layout):
     import torch
-    w = wl.CONFIGS[cfg]
+    w = wl.WORKLOADS[cfg]
     log(f"case full config {cfg} ({w.name}) steps={steps} layout={layout}")
     run = GpuRun(w, layout)
     run.run(steps)
@@ -360,9 +360,9 @@ def test_full_size_config_windows(cfg, steps, layout):
 @pytest.mark.parametrize("name", [n for n in wl.SCHEDULE_VARIANTS if n != "random_gb"])
 def test_full_size_schedule_variants(name):
     import torch
-    w = wl.with_schedule(wl.CONFIGS[4], name)
+    w = wl.with_schedule(wl.WORKLOADS[4], name)
     steps = 12
-    log(f"case full config 4 schedule={name} steps={steps}")
+    log(f"case full heterogeneous workload schedule={name} steps={steps}")
     run = GpuRun(w)
     run.run(steps)
     torch.cuda.synchronize()
@@ -370,6 +370,6 @@ def test_full_size_schedule_variants(name):
     assert run.schedule == [osch.step(t, w.eligible(t)) for t in range(steps)]
     windows = sample_windows(w.numel, 8, 1 << 15, seed=40)
     worst = check_against_oracle(run, windows, f"config4 {name}")
-    log(f"config 4 {name}: {len(windows)} windows x {w.n} replicas ok, max rel err {worst:.2e}")
+    log(f"heterogeneous {name}: {len(windows)} windows x {w.n} replicas ok, max rel err {worst:.2e}")
     del run
     torch.cuda.empty_cache()
