@@ -236,6 +236,32 @@ def test_single_replica(dtype):
     check_against_oracle(run, full_windows(w.numel), "N=1")
 
 
+@pytest.fixture
+def launch_defaults():
+    """Restores the process-wide launch settings whatever the test does."""
+    import paper_1909_08029_amd as rip
+    yield rip
+    rip.rip_set_max_blocks(0)
+    rip.rip_set_blocks_per_cu(0)
+
+
+@pytest.mark.parametrize("max_blocks,per_cu", [(1, 0), (7, 0), (1000, 0), (0, 1), (0, 3), (0, 32)])
+def test_launch_settings_do_not_change_results(launch_defaults, max_blocks, per_cu):
+    """Few workgroups looping over all tiles (the grid-stride path) and
+    residency caps from 1 to 32 workgroups per CU: same bits as the oracle,
+    on groups of many sizes, lone updates and momentum."""
+    rip = launch_defaults
+    rip.rip_set_max_blocks(max_blocks)
+    rip.rip_set_blocks_per_cu(per_cu)
+    table = [[(0, 1, 2), (3, 4), tuple(range(5, 15))], [(1, 3, 5, 7, 9, 11, 13), (0, 2)]]
+    w = wl.Workload("launch", 16, [3 * 4096 + 13, 1000], DTYPE_F32, 0.1, 0.9, 0.01,
+                    dict(mode=wl.TABLE, table=table), 4, 91, straggler_every=2, grad_ring=2)
+    log(f"case launch settings max_blocks={max_blocks} blocks_per_cu={per_cu}")
+    run = GpuRun(w)
+    run.run(w.steps)
+    check_against_oracle(run, full_windows(w.numel), f"max_blocks={max_blocks} per_cu={per_cu}")
+
+
 def test_pure_preduce_invariants_and_untouched():
     """Members end bit-identical, replicas outside every group keep their
     bytes, and the replica sum is preserved (doubly stochastic F^G)."""
