@@ -215,26 +215,27 @@ def main():
 
     def one_step(ev=None):
         nonlocal t
-        active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
-        if ev is not None:
-            stats["steps"] += 1
-            stats["updates"] += len(active)
-            stats["groups"] += sum(1 for g in groups if len(g) > 1)
-            stats["members"] += sum(len(g) for g in groups if len(g) > 1)
-            stats["empty"] += 0 if (active or any(len(g) > 1 for g in groups)) else 1
         h = handles[w.grad_slot(t)]
         opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
                    nesterov=w.nesterov)
         if ev is not None:
             ev[0].record(stream)
         if args.unfused:
+            active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
             if active:
                 rip.rip_local_step(h, active, w.lr, **opt)
             rip.rip_preduce(h, groups, stream=stream)
         else:
-            rip.rip_preduce(h, groups, active, lr=w.lr, **opt)
+            # group generation and the fused launch in one library call
+            active, groups = rip.rip_step(sched, h, t, w.lr, eligible=w.eligible(t), **opt)
         if ev is not None:
             ev[1].record(stream)
+        if ev is not None:
+            stats["steps"] += 1
+            stats["updates"] += len(active)
+            stats["groups"] += sum(1 for g in groups if len(g) > 1)
+            stats["members"] += sum(len(g) for g in groups if len(g) > 1)
+            stats["empty"] += 0 if (active or any(len(g) > 1 for g in groups)) else 1
         t += 1
         if args.unfused:
             return w.alg_bytes_unfused(active, groups)

@@ -261,6 +261,26 @@ int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offsets,
                     const int32_t* members, int32_t n_groups, const int32_t* active,
                     int32_t n_active, const rip_sgd* sgd, void* stream);
 
+/* One whole step of the algorithm of Fig. 4 for every worker in one call:
+ * group generation for `step` (Step 3, exactly as rip_schedule_groups with
+ * the same arguments), then the fused local update and P-Reduce of the
+ * groups that run (Steps 2 and 4, as rip_preduce with those groups and the
+ * active workers).  Saves the host round trip between the two calls.
+ *  s, r       scheduler and replicas handle with the same number of workers
+ *  sgd        required (the workers that finish an iteration update); the
+ *             handle needs gradient buffers, and momentum buffers when
+ *             sgd->momentum != 0
+ *  active .. n_groups  optional outputs, as in rip_schedule_groups (NULL =
+ *             not wanted); written only on success
+ * Atomic: on any error (including a failed launch) the scheduler is left as
+ * it was, as if the call had not been made, and nothing is launched.
+ * Errors: RIP_E_INVAL (null handle or sgd, worker counts differ, missing
+ * buffers, Nesterov without momentum, device mismatch, a scheduling error),
+ * RIP_E_HIP. */
+int32_t rip_step(rip_sched* s, const rip_replicas* r, int64_t step, const uint8_t* eligible,
+                 const rip_sgd* sgd, void* stream, int32_t* active, int32_t* n_active,
+                 int32_t* group_offsets, int32_t* members, int32_t* n_groups);
+
 /* Launch tuning (process-wide).  rip_set_max_blocks caps the workgroups of
  * one launch (0 = one workgroup per tile); rip_set_blocks_per_cu caps how
  * many of the kernel's workgroups share a compute unit (0 = the library's

@@ -92,6 +92,9 @@ def _load():
         "rip_local_step": (ctypes.c_int32, [vp, _i32p, ctypes.c_int32, ctypes.POINTER(Sgd), vp]),
         "rip_preduce": (ctypes.c_int32, [vp, _i32p, _i32p, ctypes.c_int32, _i32p,
                                          ctypes.c_int32, ctypes.POINTER(Sgd), vp]),
+        "rip_step": (ctypes.c_int32, [vp, vp, ctypes.c_int64, ctypes.c_char_p,
+                                      ctypes.POINTER(Sgd), vp, _i32p, _i32p, _i32p, _i32p,
+                                      _i32p]),
         "rip_set_max_blocks": (ctypes.c_int32, [ctypes.c_int32]),
         "rip_set_blocks_per_cu": (ctypes.c_int32, [ctypes.c_int32]),
     }
@@ -279,6 +282,24 @@ def rip_preduce(rep: Replicas, groups: Sequence[Sequence[int]], active: Sequence
         Sgd(lr, momentum, weight_decay, int(bool(nesterov))))
     _check(lib.rip_preduce(rep._h, off, mem, len(groups), act, len(active), sgd,
                            _stream_ptr(stream)))
+
+
+def rip_step(sched: Scheduler, rep: Replicas, step: int, lr: float, momentum: float = 0.0,
+             eligible: Optional[Sequence[bool]] = None, stream=None, weight_decay: float = 0.0,
+             nesterov: bool = False) -> Tuple[List[int], List[Tuple[int, ...]]]:
+    """Group generation for ``step`` and the fused launch in one call (see
+    include/rip.h).  Returns (active ids, groups) as rip_schedule_groups."""
+    el = None if eligible is None else bytes(1 if e else 0 for e in eligible)
+    if el is not None and len(el) != sched.n:
+        raise ValueError("eligible must have one entry per worker")
+    sgd = Sgd(lr, momentum, weight_decay, int(bool(nesterov)))
+    _check(lib.rip_step(sched._h, rep._h, step, el, ctypes.byref(sgd), _stream_ptr(stream),
+                        sched._act, ctypes.byref(sched._na), sched._off, sched._mem,
+                        ctypes.byref(sched._ng)))
+    active = list(sched._act[:sched._na.value])
+    off = sched._off[:sched._ng.value + 1]
+    groups = [tuple(sched._mem[off[g]:off[g + 1]]) for g in range(sched._ng.value)]
+    return active, groups
 
 
 def rip_set_max_blocks(n: int) -> None:

@@ -364,6 +364,43 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   return RIP_OK;
 }
 
+extern "C" int32_t rip_step(rip_sched* s, const rip_replicas* r, int64_t step,
+                            const uint8_t* eligible, const rip_sgd* sgd, void* stream,
+                            int32_t* active, int32_t* n_active, int32_t* group_offsets,
+                            int32_t* members, int32_t* n_groups) {
+  rip::clear_error();
+  if (!s || !r || !sgd) return rip::fail(RIP_E_INVAL, "rip_step: null scheduler, replicas or sgd");
+  if (rip::sched_workers(s) != r->n)
+    return rip::fail(RIP_E_INVAL, "scheduler has %d workers, replicas handle %d",
+                     rip::sched_workers(s), r->n);
+  // Everything the launch could reject for any schedule is checked before
+  // the scheduler moves.
+  if (!r->has_grad) return rip::fail(RIP_E_INVAL, "rip_step: replicas have no gradient buffers");
+  if (sgd->momentum != 0.0f && !r->has_mom)
+    return rip::fail(RIP_E_INVAL, "momentum %g without momentum buffers", (double)sgd->momentum);
+  if (sgd->nesterov && sgd->momentum == 0.0f)
+    return rip::fail(RIP_E_INVAL, "Nesterov momentum needs a nonzero momentum");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return rip::fail(RIP_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev != r->device)
+    return rip::fail(RIP_E_INVAL, "current device %d differs from the handle's device %d", dev,
+                     r->device);
+  int32_t act_buf[RIP_MAX_REPLICAS], off_buf[RIP_MAX_REPLICAS + 1], mem_buf[RIP_MAX_REPLICAS];
+  int32_t na = 0, ng = 0;
+  int32_t* act = active ? active : act_buf;
+  int32_t* off = group_offsets ? group_offsets : off_buf;
+  int32_t* mem = members ? members : mem_buf;
+  const int32_t rc = rip::schedule_then(s, step, eligible, act, &na, off, mem, &ng, [&] {
+    return rip_preduce(r, off, mem, ng, act, na, sgd, stream);
+  });
+  if (rc == RIP_OK) {
+    if (n_active) *n_active = na;
+    if (n_groups) *n_groups = ng;
+  }
+  return rc;
+}
+
 extern "C" int32_t rip_local_step(const rip_replicas* r, const int32_t* active, int32_t n_active,
                                   const rip_sgd* sgd, void* stream) {
   if (!sgd) {

@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <cstring>
 #include <deque>
+#include <functional>
 #include <map>
 #include <new>
 #include <vector>
@@ -431,17 +432,12 @@ extern "C" int32_t rip_sched_create(const rip_sched_cfg* cfg, rip_sched** out) {
 
 extern "C" void rip_sched_destroy(rip_sched* s) { delete s; }
 
-extern "C" int32_t rip_schedule_groups(rip_sched* s, int64_t step, const uint8_t* eligible,
-                                       int32_t* active, int32_t* n_active, int32_t* group_offsets,
-                                       int32_t* members, int32_t* n_groups) {
-  rip::clear_error();
-  if (!s || !active || !n_active || !group_offsets || !members || !n_groups)
-    return rip::fail(RIP_E_INVAL, "rip_schedule_groups: null argument");
-  if (step != s->st.t)
-    return rip::fail(RIP_E_INVAL, "steps must be consecutive: expected %lld, got %lld",
-                     (long long)s->st.t, (long long)step);
+namespace {
+
+// One step of group generation on s->st (the caller restores it on error).
+int32_t schedule_step(rip_sched* s, const uint8_t* eligible, int32_t* active, int32_t* n_active,
+                      int32_t* group_offsets, int32_t* members, int32_t* n_groups) {
   const int n = s->n;
-  rip_sched::State saved = s->st;  // a failed step leaves no trace
   s->st.t += 1;
 
   int32_t na = 0;
@@ -453,10 +449,7 @@ extern "C" int32_t rip_schedule_groups(rip_sched* s, int64_t step, const uint8_t
   }
   for (int32_t a = 0; a < na; ++a) {
     int32_t rc = s->request(active[a]);
-    if (rc != RIP_OK) {
-      s->st = std::move(saved);
-      return rc;
-    }
+    if (rc != RIP_OK) return rc;
   }
   // Groups whose every member is blocked on them, in id order.
   std::vector<int64_t> ready;
@@ -489,6 +482,37 @@ extern "C" int32_t rip_schedule_groups(rip_sched* s, int64_t step, const uint8_t
   *n_active = na;
   *n_groups = ng;
   return RIP_OK;
+}
+
+}  // namespace
+
+namespace rip {
+
+int32_t sched_workers(const rip_sched* s) { return s->n; }
+
+int32_t schedule_then(rip_sched* s, int64_t step, const uint8_t* eligible, int32_t* active,
+                      int32_t* n_active, int32_t* group_offsets, int32_t* members,
+                      int32_t* n_groups, const std::function<int32_t()>& then) {
+  if (step != s->st.t)
+    return fail(RIP_E_INVAL, "steps must be consecutive: expected %lld, got %lld",
+                (long long)s->st.t, (long long)step);
+  rip_sched::State saved = s->st;  // a failed step leaves no trace
+  int32_t rc = schedule_step(s, eligible, active, n_active, group_offsets, members, n_groups);
+  if (rc == RIP_OK && then) rc = then();
+  if (rc != RIP_OK) s->st = std::move(saved);
+  return rc;
+}
+
+}  // namespace rip
+
+extern "C" int32_t rip_schedule_groups(rip_sched* s, int64_t step, const uint8_t* eligible,
+                                       int32_t* active, int32_t* n_active, int32_t* group_offsets,
+                                       int32_t* members, int32_t* n_groups) {
+  rip::clear_error();
+  if (!s || !active || !n_active || !group_offsets || !members || !n_groups)
+    return rip::fail(RIP_E_INVAL, "rip_schedule_groups: null argument");
+  return rip::schedule_then(s, step, eligible, active, n_active, group_offsets, members, n_groups,
+                            nullptr);
 }
 
 extern "C" int32_t rip_sched_worker(const rip_sched* s, int32_t worker, rip_worker_state* out) {

@@ -163,3 +163,18 @@ def test_replicas_create_checks_before_any_device_call():
     assert lib.rip_preduce(None, None, None, 0, None, 0, None, None) == rip.RIP_E_INVAL
     sgd = rip.Sgd(0.1, 0.0, 0.0, 0)
     assert lib.rip_local_step(None, None, 0, ctypes.byref(sgd), None) == rip.RIP_E_INVAL
+
+
+def test_step_rejects_null_handles_and_leaves_the_scheduler():
+    lib = rip.lib
+    s = rip.Scheduler(4, rip.SCHED_STATIC, seed=2, group_size=2, period=4)
+    sgd = rip.Sgd(0.1, 0.0, 0.0, 0)
+    assert lib.rip_step(s._h, None, 0, None, ctypes.byref(sgd), None,
+                        None, None, None, None, None) == rip.RIP_E_INVAL
+    assert lib.rip_step(None, None, 0, None, ctypes.byref(sgd), None,
+                        None, None, None, None, None) == rip.RIP_E_INVAL
+    assert lib.rip_step(s._h, None, 0, None, None, None,
+                        None, None, None, None, None) == rip.RIP_E_INVAL
+    # the scheduler did not move: step 0 is still the next step
+    fresh = rip.Scheduler(4, rip.SCHED_STATIC, seed=2, group_size=2, period=4)
+    assert rip.rip_schedule_groups(s, 0) == rip.rip_schedule_groups(fresh, 0)

@@ -399,3 +399,59 @@ def test_full_size_schedule_variants(name):
     log(f"heterogeneous {name}: {len(windows)} windows x {w.n} replicas ok, max rel err {worst:.2e}")
     del run
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# rip_step: group generation and the fused launch in one call
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+def test_step_equals_schedule_then_preduce(dtype):
+    """rip_step on one copy, rip_schedule_groups + rip_preduce on another:
+    same schedules, same bits after every step, and the oracle's result."""
+    import torch
+    import paper_1909_08029_amd as rip
+    w = wl.scaled(wl.WORKLOADS[4], [3 * 4096 + 17], steps=12, n=12, dtype=dtype,
+                  lr=0.1 if dtype == DTYPE_F32 else 20.0, momentum=0.9,
+                  param_sigma=1.0 if dtype == DTYPE_F32 else 0.05,
+                  sched=dict(mode=wl.GD, seed=12, kmin=2, kmax=9, c_thres=3))
+    log(f"case rip_step dtype={dtype}")
+    a, b = GpuRun(w), GpuRun(w)
+    view = np.uint16 if dtype == DTYPE_BF16 else np.uint32
+    for t in range(w.steps):
+        h = a.handles[w.grad_slot(t)]
+        got = rip.rip_step(a.sched, h, t, w.lr, w.momentum, eligible=w.eligible(t))
+        a.schedule.append(got)
+        b.step()
+        assert got == b.schedule[-1], f"step {t}"
+        torch.cuda.synchronize()
+        for r in range(w.n):
+            assert np.array_equal(a.state.window("param", r, 0, w.numel).view(view),
+                                  b.state.window("param", r, 0, w.numel).view(view)), (t, r)
+    check_against_oracle(a, full_windows(w.numel), "rip_step")
+
+
+def test_step_failure_leaves_scheduler_and_memory():
+    """Rejected rip_step calls (momentum without momentum buffers, handles of
+    different sizes) launch nothing and leave the scheduler at the same step."""
+    import torch
+    import paper_1909_08029_amd as rip
+    w = wl.scaled(wl.WORKLOADS[4], [4099], steps=2, n=6, momentum=0.0,
+                  sched=dict(mode=wl.RANDOM_GB, seed=13, kmin=2, kmax=4))
+    run = GpuRun(w)
+    before = [run.state.window("param", r, 0, w.numel).copy() for r in range(w.n)]
+    h = run.handles[0]
+    with pytest.raises(rip.RipError) as e:
+        rip.rip_step(run.sched, h, 0, 0.1, momentum=0.9)       # no momentum buffers
+    assert e.value.code == rip.RIP_E_INVAL
+    other = wl.DeviceState(wl.scaled(w, [4099], n=5))
+    other.fill()
+    h5 = rip.Replicas(other.param, other.grad_sets[0], None)
+    with pytest.raises(rip.RipError) as e:
+        rip.rip_step(run.sched, h5, 0, 0.1)                    # 5 replicas, 6 workers
+    assert e.value.code == rip.RIP_E_INVAL
+    torch.cuda.synchronize()
+    for r in range(w.n):
+        assert np.array_equal(run.state.window("param", r, 0, w.numel).view(np.uint32),
+                              before[r].view(np.uint32))
+    osch = oracle_scheduler(w)
+    assert rip.rip_step(run.sched, h, 0, w.lr) == osch.step(0, None)
