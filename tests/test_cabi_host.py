@@ -178,3 +178,71 @@ def test_step_rejects_null_handles_and_leaves_the_scheduler():
     # the scheduler did not move: step 0 is still the next step
     fresh = rip.Scheduler(4, rip.SCHED_STATIC, seed=2, group_size=2, period=4)
     assert rip.rip_schedule_groups(s, 0) == rip.rip_schedule_groups(fresh, 0)
+
+
+def _random_sched_case(seed):
+    """A random scheduler configuration (any mode) with random eligibility."""
+    import numpy as np
+    rs = np.random.default_rng(seed)
+    mode = int(rs.choice([os_.TABLE, os_.STATIC, os_.RANDOM_GB, os_.GD, os_.RULE,
+                          os_.INTER_INTRA, os_.ADPSGD]))
+    kw = {}
+    if mode == os_.RULE:
+        nodes = int(rs.choice([1, 2, 4, 6]))
+        n, kw = 4 * nodes, dict(n_nodes=nodes)
+    elif mode == os_.INTER_INTRA:
+        nodes = int(rs.integers(1, 6))
+        n = nodes * int(rs.integers(1, 7))
+        kmin = int(rs.integers(1, 5))
+        kw = dict(seed=int(rs.integers(0, 2 ** 63)), kmin=kmin, kmax=kmin + int(rs.integers(0, 5)),
+                  c_thres=int(rs.integers(0, 5)), n_nodes=nodes)
+    elif mode == os_.STATIC:
+        k = int(rs.integers(2, 6))
+        n = k * int(rs.integers(1, 8))
+        kw = dict(seed=int(rs.integers(0, 2 ** 63)), group_size=k, period=int(rs.integers(1, 6)))
+    elif mode == os_.TABLE:
+        n = int(rs.integers(1, 30))
+        table = []
+        for _ in range(int(rs.integers(1, 4))):
+            order = [int(x) for x in rs.permutation(n)][:int(rs.integers(0, n + 1))]
+            row, i = [], 0
+            while i < len(order):
+                k = int(rs.integers(1, len(order) - i + 1))
+                row.append(tuple(sorted(order[i:i + k])))
+                i += k
+            table.append(row)
+        kw = dict(table=table)
+    else:
+        n = int(rs.integers(1, 40))
+        kmin = int(rs.integers(1, 6))
+        kw = dict(seed=int(rs.integers(0, 2 ** 63)), kmin=kmin, kmax=kmin + int(rs.integers(0, 6)))
+        if mode == os_.GD:
+            kw["c_thres"] = int(rs.integers(0, 6))
+        if mode == os_.ADPSGD:
+            kw = dict(seed=kw["seed"])
+    p_eligible = float(rs.choice([1.0, 0.9, 0.6, 0.3]))
+    masks = [[bool(x) for x in rs.random(n) < p_eligible] for _ in range(300)]
+    return n, mode, kw, masks
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_scheduler_parity_random_configurations(seed):
+    """C++ scheduler = oracle scheduler on random configurations of every mode
+    with random per-step eligibility, 300 steps, including the per-worker
+    counters."""
+    n, mode, kw, masks = _random_sched_case(seed)
+    bkw = dict(kw)
+    try:
+        o = os_.Scheduler(n, mode, **kw)
+    except ValueError:
+        with pytest.raises(rip.RipError):
+            rip.Scheduler(n, mode, **bkw)
+        return
+    c = rip.Scheduler(n, mode, **bkw)
+    for t, el in enumerate(masks):
+        assert rip.rip_schedule_groups(c, t, el) == o.step(t, el), f"mode {mode} step {t}"
+    for i in range(n):
+        ws = c.worker(i)
+        depth = int(o.waiting[i]) if o.mode == os_.ADPSGD else len(o.gb[i])
+        assert (ws.requests, ws.syncs, ws.skips, bool(ws.waiting), ws.gb_depth) == \
+            (o.c[i], o.syncs[i], o.skips[i], o.waiting[i], depth)
