@@ -225,7 +225,7 @@ def _random_sched_case(seed):
     return n, mode, kw, masks
 
 
-@pytest.mark.parametrize("seed", range(60))
+@pytest.mark.parametrize("seed", range(150))
 def test_scheduler_parity_random_configurations(seed):
     """C++ scheduler = oracle scheduler on random configurations of every mode
     with random per-step eligibility, 300 steps, including the per-worker
