@@ -18,7 +18,7 @@ from gpu_util import GpuRun, check_against_oracle, log
 
 pytestmark = pytest.mark.gpu
 
-CASES = 48
+CASES = 96
 
 
 def _random_rows(rs, n, rows=2):
