@@ -43,31 +43,33 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Replica buffers are plain device memory: access them through the global
-// address space so the compiler emits global_* (not flat_*) instructions.
+// Replica buffers are plain device memory: the element-wise path (ragged
+// tails) accesses them through the global address space so the compiler
+// emits global_* (not flat_*) instructions.
 #define RIP_GLOBAL __attribute__((address_space(1)))
 
-// Streaming hints: every byte is touched once per step.
-#ifndef RIP_NT_LOAD
-#define RIP_NT_LOAD 1
-#endif
-#ifndef RIP_NT_STORE
-#define RIP_NT_STORE 1
-#endif
+// Full tiles are accessed through buffer instructions, non-temporal (every
+// byte is touched once per step): a descriptor per member stream whose base
+// is the tile's first byte and whose size is the tile's bytes, and a
+// per-lane offset of at most a few KB.  On gfx950 this form streamed 3-4%
+// faster than the same non-temporal accesses as global instructions (with a
+// 64-bit per-lane address or an SGPR base and 32-bit offset alike), and
+// faster than a buffer descriptor over the whole stream with the tile offset
+// folded into the per-lane offset.  The descriptor's size also bounds every
+// access in hardware.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;  // raw (untyped) buffer, 32-bit data format
+constexpr int kNonTemporal = 2;         // cache-policy operand: nt
 
-__device__ __forceinline__ u32x4 ld16(const char* p) {
-#if RIP_NT_LOAD
-  return __builtin_nontemporal_load((const RIP_GLOBAL u32x4*)p);
-#else
-  return *(const RIP_GLOBAL u32x4*)p;
-#endif
+__device__ __forceinline__ Rsrc tile_rsrc(const char* base, int64_t tile_byte, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base) + tile_byte, 0, bytes,
+                                           kRsrcWord3);
 }
-__device__ __forceinline__ void st16(char* p, u32x4 v) {
-#if RIP_NT_STORE
-  __builtin_nontemporal_store(v, (RIP_GLOBAL u32x4*)p);
-#else
-  *(RIP_GLOBAL u32x4*)p = v;
-#endif
+__device__ __forceinline__ u32x4 bld16(Rsrc r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
+}
+__device__ __forceinline__ void bst16(Rsrc r, int off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kNonTemporal);
 }
 
 // The launch tables (the kernel argument's arrays, the registered pointer and
@@ -254,22 +256,33 @@ __device__ __forceinline__ void load_members(const StepArgs& a, uint64_t ids, ui
   }
 }
 
-// U consecutive 16-byte slots of a full tile for a unit of K members.
+// U consecutive 16-byte slots of a full tile for a unit of K members; the
+// tile starts `tile_byte` bytes into every member stream.
 template <int K, int U, bool BF16, bool MOM, bool EXT>
-__device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off)[U],
-                                           const Opt& o) {
+__device__ __forceinline__ void tile_slots(const Members& m, int64_t tile_byte, const Opt& o) {
   using V = Vec<BF16>;
   constexpr int N = V::N;
   constexpr float inv_k = (float)(1.0 / K);
+  constexpr int kTileBytes = U * kBlock * 16;
+  int off[U];  // this lane's byte offset of each slot within the tile
+#pragma unroll
+  for (int u = 0; u < U; ++u) off[u] = (u * kBlock + (int)threadIdx.x) * 16;
+  Rsrc rw[K], rg[K], rv[K];
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    rw[j] = tile_rsrc(m.w[j], tile_byte, kTileBytes);
+    rg[j] = tile_rsrc(m.g[j], tile_byte, kTileBytes);
+    if constexpr (MOM) rv[j] = tile_rsrc(m.v[j], tile_byte, kTileBytes);
+  }
   u32x4 wv[U][K], gv[U][K], vv[U][K];
 #pragma unroll
   for (int u = 0; u < U; ++u)
 #pragma unroll
     for (int j = 0; j < K; ++j) {
-      wv[u][j] = ld16(m.w[j] + off[u]);
+      wv[u][j] = bld16(rw[j], off[u]);
       if (m.act[j]) {
-        gv[u][j] = ld16(m.g[j] + off[u]);
-        if constexpr (MOM) vv[u][j] = ld16(m.v[j] + off[u]);
+        gv[u][j] = bld16(rg[j], off[u]);
+        if constexpr (MOM) vv[u][j] = bld16(rv[j], off[u]);
       }
     }
   // All arithmetic comes before the first store.  Stores count against the
@@ -311,12 +324,12 @@ __device__ __forceinline__ void tile_slots(const Members& m, const int64_t (&off
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int j = 0; j < K; ++j)
-        if (m.act[j]) st16(m.v[j] + off[u], vv[u][j]);
+        if (m.act[j]) bst16(rv[j], off[u], vv[u][j]);
   }
 #pragma unroll
   for (int u = 0; u < U; ++u)
 #pragma unroll
-    for (int j = 0; j < K; ++j) st16(m.w[j] + off[u], out[u]);
+    for (int j = 0; j < K; ++j) bst16(rw[j], off[u], out[u]);
 }
 
 // Element-wise path for a partial tile (any k): each thread walks elements
@@ -370,7 +383,9 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
   constexpr int C = kMaxK;  // members per chunk
   const int plane = a.n_seg * a.n_rep;
   const Opt o{a.lr, a.mu, a.wd, a.nesterov != 0};
-  const int64_t off = (e_tile + (int64_t)threadIdx.x * N) * (BF16 ? 2 : 4);
+  const int64_t tile_byte = e_tile * (BF16 ? 2 : 4);
+  constexpr int kTileBytes = kBlock * 16;
+  const int off = (int)threadIdx.x * 16;
   float s[N];
   for (int j0 = 0; j0 < k; j0 += C) {
     const uint64_t ids = cld8x8(a.member, base + j0);  // bytes past the unit are unused
@@ -393,14 +408,21 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
       asm volatile("" ::"s"(w[jj]), "s"(g[jj]), "s"((int)act[jj]));
       if constexpr (MOM) asm volatile("" ::"s"(v[jj]));
     }
+    Rsrc rw[C], rg[C], rv[C];
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) {
+      rw[jj] = tile_rsrc(w[jj], tile_byte, kTileBytes);
+      rg[jj] = tile_rsrc(g[jj], tile_byte, kTileBytes);
+      if constexpr (MOM) rv[jj] = tile_rsrc(v[jj], tile_byte, kTileBytes);
+    }
     u32x4 wv[C], gv[C], vv[C];
 #pragma unroll
     for (int jj = 0; jj < C; ++jj) {
       if (j0 + jj < k) {
-        wv[jj] = ld16(w[jj] + off);
+        wv[jj] = bld16(rw[jj], off);
         if (act[jj]) {
-          gv[jj] = ld16(g[jj] + off);
-          if constexpr (MOM) vv[jj] = ld16(v[jj] + off);
+          gv[jj] = bld16(rg[jj], off);
+          if constexpr (MOM) vv[jj] = bld16(rv[jj], off);
         }
       }
     }
@@ -425,7 +447,7 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
     if constexpr (MOM) {
 #pragma unroll
       for (int jj = 0; jj < C; ++jj)
-        if (act[jj]) st16(v[jj] + off, vv[jj]);
+        if (act[jj]) bst16(rv[jj], off, vv[jj]);
     }
   }
   const float inv_k = kInv.v[k];
@@ -444,7 +466,7 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
     for (int jj = 0; jj < C; ++jj) asm volatile("" ::"s"(w[jj]));
 #pragma unroll
     for (int jj = 0; jj < C; ++jj)
-      if (j0 + jj < k) st16(w[jj] + off, out);
+      if (j0 + jj < k) bst16(tile_rsrc(w[jj], tile_byte, kTileBytes), off, out);
   }
 }
 
@@ -500,11 +522,7 @@ __device__ __forceinline__ void unit_tile(const StepArgs& a, const Header& h, co
       constexpr int esize = BF16 ? 2 : 4;
       Members m;
       load_members<K, MOM>(a, u.ids, u.act8, seg, m);
-      int64_t off[SL];
-#pragma unroll
-      for (int s = 0; s < SL; ++s)
-        off[s] = (e_tile + (int64_t)(s * kBlock + (int)threadIdx.x) * N) * esize;
-      tile_slots<K, SL, BF16, MOM, EXT>(m, off, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
+      tile_slots<K, SL, BF16, MOM, EXT>(m, e_tile * esize, Opt{a.lr, a.mu, a.wd, a.nesterov != 0});
       return;
     }
   } else {
