@@ -13,6 +13,11 @@
 //            (24 reads, 16 writes), the shape of a group of eight with
 //            momentum
 //
+// group4 and group8m use the fused kernel's own access form for full tiles
+// (buffer instructions, a descriptor per stream and tile); group4-global is
+// the same shape through global instructions, and read, copy and 2R1W use
+// global instructions too.
+//
 // Every stream is 1 GiB.  The buffers are measured twice: filled with
 // random values (as the workloads are) and zero-filled, because the
 // sustained bandwidth depends on the data moved.  Standalone program; prints
@@ -21,7 +26,7 @@
 //
 // With the argument "xcd" it instead measures XCD-aware tile placement:
 // it prints the XCD (hardware XCC_ID register) each of the first 64
-// workgroups runs on, then times the read, copy and group4 streams with the
+// workgroups runs on, then times the read, copy and group4-global streams with the
 // tiles permuted over workgroups so that XCD x (workgroup b runs on XCD
 // b mod 8) handles the tiles whose chunk index (tile / C) is congruent to
 // x + s mod 8, for chunk sizes C of 1 to 2048 tiles, or a contiguous eighth
@@ -65,7 +70,26 @@ __device__ __forceinline__ uint32_t place(const Streams& s, uint32_t b, uint32_t
   return b;
 }
 
-enum Kind { kRead = 0, kCopy = 1, k2R1W = 2, kGroup4 = 3, kGroup8Mom = 4 };
+enum Kind { kRead = 0, kCopy = 1, k2R1W = 2, kGroup4 = 3, kGroup8Mom = 4, kGroup4Buf = 5,
+            kGroup8MomBuf = 6 };
+
+// The buffer form of the fused kernel's full tiles: a descriptor per stream
+// whose base is the tile's first byte and whose size is the tile, lanes
+// addressing it with a small offset; non-temporal.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ Rsrc tile_rsrc(char* base, uint32_t t) {
+  return __builtin_amdgcn_make_buffer_rsrc(base + (int64_t)t * kLanes * 16, 0, kLanes * 16,
+                                           0x00020000);
+}
+__device__ __forceinline__ f32x4 bload(Rsrc r) {
+  return __builtin_bit_cast(
+      f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)threadIdx.x * 16, 0, 2));
+}
+__device__ __forceinline__ void bstore(Rsrc r, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)threadIdx.x * 16,
+                                         0, 2);
+}
 
 template <int KIND>
 __global__ __launch_bounds__(kLanes) void stream_kernel(Streams s) {
@@ -83,6 +107,44 @@ __global__ __launch_bounds__(kLanes) void stream_kernel(Streams s) {
     }
     // never true for the fills used here; keeps the loads live
     if (acc.x == 1234.5f && acc.y == -1234.5f) store_nt(s.p[1] + threadIdx.x * 16, acc);
+  } else if constexpr (KIND == kGroup4Buf) {
+    Rsrc r[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r[j] = tile_rsrc(s.p[j], t);
+    f32x4 w[4], g[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      w[j] = bload(r[j]);
+      g[j] = bload(r[4 + j]);
+    }
+    f32x4 sum = w[0] - s.lr * g[0];
+#pragma unroll
+    for (int j = 1; j < 4; ++j) sum = sum + (w[j] - s.lr * g[j]);
+    sum = sum * 0.25f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bstore(r[j], sum);
+  } else if constexpr (KIND == kGroup8MomBuf) {
+    Rsrc r[24];
+#pragma unroll
+    for (int j = 0; j < 24; ++j) r[j] = tile_rsrc(s.p[j], t);
+    f32x4 w[8], g[8], v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      w[j] = bload(r[j]);
+      g[j] = bload(r[8 + j]);
+      v[j] = bload(r[16 + j]);
+    }
+    f32x4 sum = {0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = 0.9f * v[j] + g[j];
+      sum = sum + (w[j] - s.lr * v[j]);
+    }
+    sum = sum * 0.125f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) bstore(r[16 + j], v[j]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) bstore(r[j], sum);
   } else {
     const int64_t off = ((int64_t)t * kLanes + threadIdx.x) * 16;
     if constexpr (KIND == kCopy) {
@@ -206,7 +268,7 @@ int xcd_sweep(Streams s, int lds_per_cu, double gb) {
       const double t_g4 = time_ms<kGroup4>(x, lds);
       if (t_read < 0 || t_copy < 0 || t_g4 < 0) return 1;
       std::printf("waves/CU=%-3s placement=%s chunk=%-4u shift=%u  read %7.1f  copy %7.1f  "
-                  "group4 %7.1f GB/s\n",
+                  "group4-global %7.1f GB/s\n",
                   waves ? "10" : "max",
                   x.mode == 0 ? "identity" : (x.mode == 1 ? "chunks  " : "eighths "), x.chunk,
                   x.shift, gb / t_read * 1e3, 2 * gb / t_copy * 1e3, 12 * gb / t_g4 * 1e3);
@@ -263,15 +325,16 @@ int main(int argc, char** argv) {
       const size_t lds = waves ? ((size_t)(lds_per_cu / waves) & ~(size_t)255) : 0;
       const double t_read = time_ms<kRead>(s, lds), t_copy = time_ms<kCopy>(s, lds);
       const double t_2r1w = time_ms<k2R1W>(s, lds), t_g4 = time_ms<kGroup4>(s, lds);
-      const double t_g8m = time_ms<kGroup8Mom>(s, lds);
-      if (t_read < 0 || t_copy < 0 || t_2r1w < 0 || t_g4 < 0 || t_g8m < 0) return 1;
+      const double t_g4b = time_ms<kGroup4Buf>(s, lds);
+      const double t_g8m = time_ms<kGroup8MomBuf>(s, lds);
+      if (t_read < 0 || t_copy < 0 || t_2r1w < 0 || t_g4 < 0 || t_g4b < 0 || t_g8m < 0) return 1;
       char cap[16];
       std::snprintf(cap, sizeof cap, "%d", waves);
-      std::printf("data=%-6s waves/CU=%-4s read %7.1f  copy %7.1f  2R1W %7.1f  group4 %7.1f  "
-                  "group8m %7.1f GB/s\n",
+      std::printf("data=%-6s waves/CU=%-4s read %7.1f  copy %7.1f  2R1W %7.1f  group4-global %7.1f  "
+                  "group4 %7.1f  group8m %7.1f GB/s\n",
                   random ? "random" : "zero", waves ? cap : "max", gb / t_read * 1e3,
                   2 * gb / t_copy * 1e3, 3 * gb / t_2r1w * 1e3, 12 * gb / t_g4 * 1e3,
-                  40 * gb / t_g8m * 1e3);
+                  12 * gb / t_g4b * 1e3, 40 * gb / t_g8m * 1e3);
       std::fflush(stdout);
     }
   }
