@@ -204,11 +204,17 @@ int32_t rip_sched_worker(const rip_sched* s, int32_t worker, rip_worker_state* o
  * likewise for grad and mom), they are treated as one flat range and only
  * its first segment must be 16-byte aligned; otherwise every non-empty
  * segment must be.  Zero-length segments may be NULL.
+ * Every non-empty segment must be device (or managed) memory of the current
+ * device and lie inside the allocation holding its first byte; the buffers a
+ * step writes (param, mom) must not overlap any other registered segment.
+ * Gradient segments may overlap each other (replicas may share a gradient).
  * The handle copies the pointer table to device memory (one allocation,
  * freed by rip_replicas_destroy) on the current device; calls using it must
  * run with that device current.  Destroy only after the work that uses it
  * has finished.
- * Errors: RIP_E_INVAL, RIP_E_ALIGN, RIP_E_UNSUPPORTED (dtype, N above
+ * Errors: RIP_E_INVAL (also: not device memory of this device, or a
+ * segment running past its allocation), RIP_E_ALIGN, RIP_E_OVERLAP (a
+ * written segment overlapping another), RIP_E_UNSUPPORTED (dtype, N above
  * RIP_MAX_REPLICAS), RIP_E_NOMEM, RIP_E_HIP. */
 typedef struct rip_replicas rip_replicas; /* opaque, library-owned */
 

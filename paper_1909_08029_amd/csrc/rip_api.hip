@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstdarg>
 #include <cstdio>
@@ -125,6 +126,85 @@ int32_t check_align(void* const* p, const char* what, int32_t n, int32_t S, cons
   return RIP_OK;
 }
 
+// A registered range of one buffer kind.
+struct Range {
+  uintptr_t begin, end;
+  bool written;  // param and mom are written by a step; grad only read
+  const char* what;
+  int32_t r, s;
+};
+
+// Every non-empty segment must be memory of `device` that the kernel can
+// address (device or managed memory, not a host pointer), must lie inside
+// the allocation that holds its first byte, and the buffers a step writes
+// must overlap no other registered buffer.  Gradient buffers may overlap
+// each other (several replicas may read one gradient).  A kernel that
+// touches memory outside an allocation faults the GPU, and aliasing makes a
+// step's result depend on the order of its memory accesses, so both are
+// rejected here, once, instead of being left to the launches.
+int32_t check_buffers(void* const* param, void* const* grad, void* const* mom, int32_t n,
+                      int32_t S, const int64_t* numel, int esize, int device) {
+  std::vector<Range> ranges;
+  const struct {
+    void* const* p;
+    const char* what;
+    bool written;
+  } kinds[3] = {{param, "param", true}, {grad, "grad", false}, {mom, "mom", true}};
+  for (const auto& k : kinds) {
+    if (!k.p) continue;
+    for (int32_t r = 0; r < n; ++r)
+      for (int32_t s = 0; s < S; ++s) {
+        if (numel[s] == 0) continue;
+        void* q = k.p[(size_t)r * S + s];
+        hipPointerAttribute_t attr{};
+        hipError_t e = hipPointerGetAttributes(&attr, q);
+        if (e != hipSuccess) {
+          (void)hipGetLastError();  // leave no sticky error for the caller's next check
+          return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] = %p is not device memory (%s)", k.what, r,
+                           s, q, hipGetErrorString(e));
+        }
+        if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
+          return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] = %p is not device memory (type %d)",
+                           k.what, r, s, q, (int)attr.type);
+        if (attr.type == hipMemoryTypeDevice && attr.device != device)
+          return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] is on device %d, the current device is %d",
+                           k.what, r, s, attr.device, device);
+        const uintptr_t b = reinterpret_cast<uintptr_t>(q);
+        const uintptr_t len = (uintptr_t)numel[s] * (uintptr_t)esize;
+        hipDeviceptr_t base = nullptr;
+        size_t size = 0;
+        e = hipMemGetAddressRange(&base, &size, q);
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return rip::fail(RIP_E_INVAL, "%s[%d*S+%d] = %p: allocation not found (%s)", k.what, r,
+                           s, q, hipGetErrorString(e));
+        }
+        const uintptr_t a0 = reinterpret_cast<uintptr_t>(base);
+        if (b < a0 || b - a0 >= size || len > size - (b - a0))
+          return rip::fail(RIP_E_INVAL,
+                           "%s[%d*S+%d]: %lld elements run past the end of its allocation "
+                           "(%zu bytes from %p)",
+                           k.what, r, s, (long long)numel[s], size, base);
+        ranges.push_back({b, b + len, k.written, k.what, r, s});
+      }
+  }
+  std::sort(ranges.begin(), ranges.end(),
+            [](const Range& x, const Range& y) { return x.begin < y.begin; });
+  // Sweep in address order, remembering the furthest-reaching range seen so
+  // far and the furthest-reaching written one.
+  const Range* far_all = nullptr;
+  const Range* far_written = nullptr;
+  for (const Range& x : ranges) {
+    const Range* hit = x.written ? far_all : far_written;
+    if (hit && x.begin < hit->end)
+      return rip::fail(RIP_E_OVERLAP, "%s[%d*S+%d] overlaps %s[%d*S+%d]", x.what, x.r, x.s,
+                       hit->what, hit->r, hit->s);
+    if (!far_all || x.end > far_all->end) far_all = &x;
+    if (x.written && (!far_written || x.end > far_written->end)) far_written = &x;
+  }
+  return RIP_OK;
+}
+
 }  // namespace
 
 extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, int32_t dtype,
@@ -162,6 +242,12 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
     return rc;
   if (mom && (rc = check_align(mom, "mom", n_replicas, n_segments, seg_numel, flat)) != RIP_OK)
     return rc;
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return rip::fail(RIP_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if ((rc = check_buffers(param, grad, mom, n_replicas, n_segments, seg_numel, esize, device)) !=
+      RIP_OK)
+    return rc;
   const int32_t S = flat ? 1 : n_segments;
   const int32_t N = n_replicas;
   std::vector<uint64_t> ptab((size_t)3 * S * N, 0);
@@ -198,10 +284,9 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   h->has_mom = mom != nullptr;
   for (int o = 0; o < rip::kTileOptions; ++o) h->tiles[o] = tile0[(size_t)o * (S + 1) + S];
   h->numel0 = numel[0];
-  hipError_t e = hipGetDevice(&h->device);
-  if (e == hipSuccess)
-    e = hipDeviceGetAttribute(&h->lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
-                              h->device);
+  h->device = device;
+  e = hipDeviceGetAttribute(&h->lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                            h->device);
   const size_t bytes_ptab = ptab.size() * sizeof(uint64_t);
   const size_t bytes = bytes_ptab + (size_t)S * 8 + tile0.size() * 8;
   if (e == hipSuccess) e = hipMalloc(&h->dmem, bytes);

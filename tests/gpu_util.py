@@ -74,7 +74,7 @@ def rip_scheduler(w: wl.Workload):
     return rip.Scheduler(w.n, mode, **kw)
 
 
-class GpuRun:
+class DeviceRun:
     """The HIP path on a workload: device state, one replicas handle per
     gradient-ring slot, the library's scheduler."""
 
@@ -138,7 +138,7 @@ def sample_windows(P: int, count: int, width: int, seed: int, must: Sequence[int
     return sorted((a, a + width) for a in starts)
 
 
-def check_against_oracle(run: GpuRun, windows, label: str):
+def check_against_oracle(run: DeviceRun, windows, label: str):
     w = run.w
     ora = oracle_windows(w, run.schedule, windows, run.fused)
     worst = 0.0

@@ -21,7 +21,7 @@ import seedgen
 from seedgen import DTYPE_BF16
 from seedgen import workloads as wl
 
-from gpu_util import GpuRun, compare, log, oracle_scheduler
+from gpu_util import DeviceRun, compare, log, oracle_scheduler
 
 pytestmark = pytest.mark.gpu
 
@@ -62,7 +62,7 @@ def test_full_coverage(cfg, steps):
     w = wl.WORKLOADS[cfg]
     log(f"case full coverage config {cfg} ({w.name}) steps={steps}")
     t0 = time.time()
-    run = GpuRun(w, "flat")
+    run = DeviceRun(w, "flat")
     run.run(steps)
     torch.cuda.synchronize()
     osch = oracle_scheduler(w)

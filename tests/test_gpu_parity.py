@@ -14,7 +14,7 @@ import pytest
 from seedgen import DTYPE_BF16, DTYPE_F32
 from seedgen import workloads as wl
 
-from gpu_util import (GpuRun, check_against_oracle, compare, log, oracle_scheduler,
+from gpu_util import (DeviceRun, check_against_oracle, compare, log, oracle_scheduler,
                       sample_windows)
 
 pytestmark = pytest.mark.gpu
@@ -50,7 +50,7 @@ def test_config1_full_trajectory():
     """N=4 fp32 replicas of 1,048,576; SGD lr 0.1; group {0,1,2}; 10 steps."""
     w = wl.WORKLOADS[1]
     log(f"case {w.name}")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(w.steps)
     osch = oracle_scheduler(w)
     assert run.schedule == [osch.step(t, w.eligible(t)) for t in range(w.steps)]
@@ -76,7 +76,7 @@ def test_every_group_size_small(dtype, P):
                        0.01, dict(mode=wl.TABLE, table=[groups]), 3, 21,
                        straggler_every=2, param_sigma=1.0 if dtype == DTYPE_F32 else 0.05)
     log(f"case all-k dtype={dtype} P={P}")
-    run = GpuRun(base)
+    run = DeviceRun(base)
     run.run(base.steps)
     check_against_oracle(run, full_windows(P), f"allk P={P}")
 
@@ -97,7 +97,7 @@ def test_large_groups_with_optimizers(dtype, wd, nesterov, mom):
                     weight_decay=wd, nesterov=nesterov)
     for layout in ("flat", "separate"):
         log(f"case wide groups dtype={dtype} wd={wd} nesterov={nesterov} mom={mom} {layout}")
-        run = GpuRun(w, layout)
+        run = DeviceRun(w, layout)
         run.run(w.steps)
         assert any(len(g) > 8 for _, gs in run.schedule for g in gs)
         check_against_oracle(run, full_windows(w.numel), f"wide {layout}")
@@ -112,7 +112,7 @@ def test_segments_with_momentum(dtype, layout):
     w = wl.scaled(wl.WORKLOADS[3], segs, steps=5, grad_ring=3,
                   dtype=dtype, lr=0.1 if dtype == DTYPE_F32 else 20.0)
     log(f"case segments layout={layout} dtype={dtype}")
-    run = GpuRun(w, layout)
+    run = DeviceRun(w, layout)
     run.run(w.steps)
     check_against_oracle(run, full_windows(w.numel), f"segments {layout}")
 
@@ -125,7 +125,7 @@ def test_unfused_local_step_then_preduce(dtype):
                   lr=0.1 if dtype == DTYPE_F32 else 30.0, momentum=0.9,
                   sched=dict(mode=wl.RANDOM_GB, seed=8, kmin=2, kmax=5))
     log(f"case unfused dtype={dtype}")
-    run = GpuRun(w, fused=False)
+    run = DeviceRun(w, fused=False)
     run.run(w.steps)
     check_against_oracle(run, full_windows(w.numel), "unfused")
 
@@ -147,7 +147,7 @@ def test_optimizer_variants(dtype, wd, nesterov, mom, fused):
                   nesterov=nesterov, sched=dict(mode=wl.RANDOM_GB, seed=9, kmin=2, kmax=8),
                   straggler_every=3, grad_ring=3)
     log(f"case optimizer dtype={dtype} wd={wd} nesterov={nesterov} mom={mom} fused={fused}")
-    run = GpuRun(w, "separate", fused=fused)
+    run = DeviceRun(w, "separate", fused=fused)
     run.run(w.steps)
     check_against_oracle(run, full_windows(w.numel), "optimizer")
 
@@ -167,7 +167,7 @@ def test_nesterov_without_momentum_is_rejected():
 def test_random_gb_straggler_small():
     w = wl.scaled(wl.WORKLOADS[4], [3 * 4096 + 17], steps=40)
     log("case random-gb small")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(w.steps)
     osch = oracle_scheduler(w)
     assert run.schedule == [osch.step(t, w.eligible(t)) for t in range(w.steps)]
@@ -182,7 +182,7 @@ def test_other_schedulers_small(mode, kw):
     n = 8
     w = wl.scaled(wl.WORKLOADS[4], [8193], steps=20, n=n, sched=dict(mode=mode, **kw))
     log(f"case scheduler mode={mode}")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(w.steps)
     check_against_oracle(run, full_windows(w.numel), f"mode{mode}")
 
@@ -196,7 +196,7 @@ def test_allreduce_and_max_replicas():
     w = wl.Workload("maxn", n, [P], DTYPE_F32, 0.1, 0.0, 0.01, dict(mode=wl.TABLE, table=table),
                     2, 31, grad_ring=1)
     log("case k=N=256")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(2)
     check_against_oracle(run, full_windows(P), "k=N")
     with pytest.raises(rip.RipError):
@@ -212,7 +212,7 @@ def test_buffers_beyond_4gib(dtype, P):
                     dict(mode=wl.TABLE, table=[[(0, 1)], [(1, 2)]]), 2, 81, grad_ring=1,
                     param_sigma=1.0 if dtype == DTYPE_F32 else 0.05)
     log(f"case buffers beyond 4 GiB dtype={dtype} P={P}")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(w.steps)
     torch.cuda.synchronize()
     boundary = (1 << 32) // w.esize
@@ -230,7 +230,7 @@ def test_single_replica(dtype):
                     0.01, dict(mode=wl.TABLE, table=[[(0,)], []]), 4, 83, grad_ring=2,
                     param_sigma=1.0 if dtype == DTYPE_F32 else 0.05)
     log(f"case single replica dtype={dtype}")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(w.steps)
     assert [a for a, _ in run.schedule] == [[0]] * 4
     check_against_oracle(run, full_windows(w.numel), "N=1")
@@ -257,7 +257,7 @@ def test_launch_settings_do_not_change_results(launch_defaults, max_blocks, per_
     w = wl.Workload("launch", 16, [3 * 4096 + 13, 1000], DTYPE_F32, 0.1, 0.9, 0.01,
                     dict(mode=wl.TABLE, table=table), 4, 91, straggler_every=2, grad_ring=2)
     log(f"case launch settings max_blocks={max_blocks} blocks_per_cu={per_cu}")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(w.steps)
     check_against_oracle(run, full_windows(w.numel), f"max_blocks={max_blocks} per_cu={per_cu}")
 
@@ -302,7 +302,7 @@ def test_bf16_update_is_applied():
     w = wl.Workload("bf16upd", n, [P], DTYPE_BF16, 100.0, 0.0, 1e-3,
                     dict(mode=wl.TABLE, table=[[(0, 1)]]), 1, 51, grad_ring=1,
                     param_sigma=0.01)
-    run = GpuRun(w)
+    run = DeviceRun(w)
     before = run.state.window("param", 2, 0, P).copy()
     run.run(1)
     torch.cuda.synchronize()
@@ -352,6 +352,85 @@ def test_error_paths_change_nothing():
     torch.cuda.synchronize()
 
 
+def _register(dtype, numel, param, grad=None, mom=None):
+    """rip_replicas_create on raw pointers; returns its status (the handle,
+    if any, is destroyed)."""
+    import ctypes
+    import paper_1909_08029_amd as rip
+    S = len(numel)
+    n = len(param) // S
+
+    def arr(xs):
+        return None if xs is None else (ctypes.c_void_p * len(xs))(*xs)
+
+    h = ctypes.c_void_p()
+    rc = rip.lib.rip_replicas_create(n, S, dtype, (ctypes.c_int64 * S)(*numel), arr(param),
+                                     arr(grad), arr(mom), ctypes.byref(h))
+    if rc == 0:
+        rip.lib.rip_replicas_destroy(h)
+    return rc
+
+
+def test_registration_checks_buffers():
+    """Registration rejects host memory, segments that run past their
+    allocation and written buffers that alias another buffer; gradients may
+    be shared.  None of the rejections leaves an error behind for torch."""
+    import torch
+    import paper_1909_08029_amd as rip
+    P = 4096
+    buf = torch.zeros(8 * P, device="cuda")
+    b = buf.data_ptr()
+    q = P * 4                                   # bytes of one segment
+    pinned = torch.zeros(P, pin_memory=True)
+    pageable = np.zeros(P, dtype=np.float32)
+    cases = [
+        ("disjoint params and grads", [P], [b, b + q], [b + 2 * q, b + 3 * q], None, rip.RIP_OK),
+        ("shared gradient", [P], [b, b + q], [b + 2 * q, b + 2 * q], None, rip.RIP_OK),
+        ("pinned host param", [P], [pinned.data_ptr()], None, None, rip.RIP_E_INVAL),
+        ("pageable host grad", [P], [b], [pageable.ctypes.data], None, rip.RIP_E_INVAL),
+        ("past the allocation", [1 << 36], [b], None, None, rip.RIP_E_INVAL),
+        ("params overlap", [P], [b, b + q // 2], None, None, rip.RIP_E_OVERLAP),
+        ("grad aliases a param", [P], [b, b + q], [b + 2 * q, b], None, rip.RIP_E_OVERLAP),
+        ("param inside a grad", [P], [b + 16, b + 2 * q], [b, b + 3 * q], None, rip.RIP_E_OVERLAP),
+        ("mom aliases a param", [P], [b, b + q], None, [b + 2 * q, b + q], rip.RIP_E_OVERLAP),
+        ("empty segment is not checked", [P, 0], [b, pageable.ctypes.data], None, None,
+         rip.RIP_OK),
+        ("segments of one replica overlap", [P, P], [b, b + q // 2], None, None,
+         rip.RIP_E_OVERLAP),
+    ]
+    for name, numel, param, grad, mom, code in cases:
+        log(f"case registration: {name}")
+        assert _register(DTYPE_F32, numel, param, grad, mom) == code, name
+    # torch's own error check after a launch still sees a clean state
+    assert float(torch.ones(1024, device="cuda").sum()) == 1024.0
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+def test_shared_gradient_equals_copies(dtype):
+    """Replicas that share one gradient buffer step exactly like replicas
+    holding copies of it."""
+    import torch
+    import paper_1909_08029_amd as rip
+    n, P = 4, 3 * 4096 + 77
+    tdt = torch.bfloat16 if dtype == DTYPE_BF16 else torch.float32
+    gen = torch.Generator().manual_seed(91)
+    p0 = [torch.randn(P, generator=gen).to(tdt).cuda() for _ in range(n)]
+    g = torch.randn(P, generator=gen).to(tdt).cuda()
+    p1 = [t.clone() for t in p0]
+    shared = rip.Replicas([[t] for t in p0], [[g] for _ in range(n)], None)
+    copies = rip.Replicas([[t] for t in p1], [[g.clone()] for _ in range(n)], None)
+    for h in (shared, copies):
+        rip.rip_preduce(h, [(0, 2, 3)], [0, 1, 3], lr=0.05)
+        rip.rip_preduce(h, [(1, 2)], [1, 2], lr=0.05)
+    torch.cuda.synchronize()
+    view = torch.int16 if dtype == DTYPE_BF16 else torch.int32
+    for a, c in zip(p0, p1):
+        assert torch.equal(a.view(view), c.view(view))
+    shared.close()
+    copies.close()
+
+
 # ---------------------------------------------------------------------------
 # the five paper-shaped workloads at full size, sampled windows
 # ---------------------------------------------------------------------------
@@ -363,7 +442,7 @@ def test_full_size_config_windows(cfg, steps, layout):
     import torch
     w = wl.WORKLOADS[cfg]
     log(f"case full config {cfg} ({w.name}) steps={steps} layout={layout}")
-    run = GpuRun(w, layout)
+    run = DeviceRun(w, layout)
     run.run(steps)
     torch.cuda.synchronize()
     osch = oracle_scheduler(w)
@@ -389,7 +468,7 @@ def test_full_size_schedule_variants(name):
     w = wl.with_schedule(wl.WORKLOADS[4], name)
     steps = 12
     log(f"case full heterogeneous workload schedule={name} steps={steps}")
-    run = GpuRun(w)
+    run = DeviceRun(w)
     run.run(steps)
     torch.cuda.synchronize()
     osch = oracle_scheduler(w)
@@ -415,7 +494,7 @@ def test_step_equals_schedule_then_preduce(dtype):
                   param_sigma=1.0 if dtype == DTYPE_F32 else 0.05,
                   sched=dict(mode=wl.GD, seed=12, kmin=2, kmax=9, c_thres=3))
     log(f"case rip_step dtype={dtype}")
-    a, b = GpuRun(w), GpuRun(w)
+    a, b = DeviceRun(w), DeviceRun(w)
     view = np.uint16 if dtype == DTYPE_BF16 else np.uint32
     for t in range(w.steps):
         h = a.handles[w.grad_slot(t)]
@@ -437,7 +516,7 @@ def test_step_failure_leaves_scheduler_and_memory():
     import paper_1909_08029_amd as rip
     w = wl.scaled(wl.WORKLOADS[4], [4099], steps=2, n=6, momentum=0.0,
                   sched=dict(mode=wl.RANDOM_GB, seed=13, kmin=2, kmax=4))
-    run = GpuRun(w)
+    run = DeviceRun(w)
     before = [run.state.window("param", r, 0, w.numel).copy() for r in range(w.n)]
     h = run.handles[0]
     with pytest.raises(rip.RipError) as e:

@@ -14,7 +14,7 @@ import pytest
 from seedgen import DTYPE_BF16, DTYPE_F32
 from seedgen import workloads as wl
 
-from gpu_util import GpuRun, check_against_oracle, log
+from gpu_util import DeviceRun, check_against_oracle, log
 
 pytestmark = pytest.mark.gpu
 
@@ -65,7 +65,7 @@ def test_random_case(case):
     log(f"case random {case}: N={w.n} segs={w.seg_numel} dtype={w.dtype} mom={w.momentum} "
         f"wd={w.weight_decay} nesterov={w.nesterov} fused={fused} layout={layout} "
         f"table={[[len(g) for g in row] for row in w.sched['table']]}")
-    run = GpuRun(w, layout, fused=fused)
+    run = DeviceRun(w, layout, fused=fused)
     run.run(w.steps)
     torch.cuda.synchronize()
     check_against_oracle(run, [(0, w.numel)], f"random case {case}")
