@@ -129,6 +129,76 @@ def cpu_baseline(w, seconds: float = 12.0):
                        f"{spent:.1f} s timed, update+average only")
 
 
+def graph_steps(args, w, rip, handles, sched, t, stream, stats):
+    """Times args.steps fused steps as replays of one captured period.
+
+    Only a schedule that repeats is replayable: the steps of one period
+    (a multiple of the gradient ring) are scheduled by the library, their
+    launches captured into a HIP graph, and a second scheduler checks that the
+    next period schedules exactly the same groups.  Every replay then runs
+    those steps, as a static schedule prescribes.  Returns (period, total
+    bytes, bytes per step, kernel ms per step, wall seconds)."""
+    import math
+    import torch
+    from seedgen import workloads as wl
+    if args.unfused or w.sched["mode"] not in (wl.TABLE, wl.STATIC, wl.RULE) \
+            or w.straggler_every is not None:
+        err("--graph needs a fused step with a fixed (table, static or rule) schedule and "
+            "no straggler")
+        sys.exit(2)
+    rows = {wl.TABLE: len(w.sched.get("table", [[]])), wl.STATIC: w.sched.get("period", 4),
+            wl.RULE: 4}[w.sched["mode"]]
+    L = rows * w.grad_ring // math.gcd(rows, w.grad_ring)
+    while L < 8 and args.steps % (2 * L) == 0:   # a few steps per replay, whole periods
+        L *= 2
+    if args.steps % L:
+        err(f"--graph replays {L} steps at a time; --steps must be a multiple of {L}")
+        sys.exit(2)
+    period = [rip.rip_schedule_groups(sched, t + i) for i in range(L)]
+    kw = dict(w.sched)
+    check = rip.Scheduler(w.n, kw.pop("mode"), **kw)
+    seen = [rip.rip_schedule_groups(check, i) for i in range(t + 2 * L)]
+    if seen[t:t + L] != period or seen[t + L:] != period:
+        err("--graph: the schedule does not repeat with the captured period")
+        sys.exit(2)
+    opt = dict(momentum=w.momentum, weight_decay=w.weight_decay, nesterov=w.nesterov)
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        cap = torch.cuda.current_stream()
+        for i, (active, groups) in enumerate(period):
+            rip.rip_preduce(handles[w.grad_slot(t + i)], groups, active, lr=w.lr, stream=cap,
+                            **opt)
+    torch.cuda.synchronize()
+    g.replay()                                     # first execution, untimed
+    torch.cuda.synchronize()
+    step_bytes = [w.alg_bytes(a, gr) for a, gr in period]
+    reps = args.steps // L
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in events:
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step_bytes, kern_ms = [], []
+    for e0, e1 in events:
+        ms = e0.elapsed_time(e1) / L               # graph time spread over its launches
+        for (active, groups), b in zip(period, step_bytes):
+            per_step_bytes.append(b)
+            kern_ms.append(ms)
+            stats["steps"] += 1
+            stats["updates"] += len(active)
+            stats["groups"] += sum(1 for x in groups if len(x) > 1)
+            stats["members"] += sum(len(x) for x in groups if len(x) > 1)
+            stats["empty"] += 0 if (active or any(len(x) > 1 for x in groups)) else 1
+    del g
+    return L, sum(per_step_bytes), per_step_bytes, kern_ms, wall
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +217,10 @@ def main():
     ap.add_argument("--unfused", action="store_true",
                     help="ablation: rip_local_step then a pure rip_preduce per step "
                          "(two passes over memory; reported with its own bytes)")
+    ap.add_argument("--graph", action="store_true",
+                    help="fixed schedules only (static, rule, table; no straggler): capture "
+                         "one period of fused steps into a HIP graph and replay it, so the "
+                         "host launches once per period instead of once per step")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM counters)")
     ap.add_argument("--ceiling", action="store_true",
@@ -246,20 +320,26 @@ def main():
     torch.cuda.synchronize()
     err(f"[bench] {args.warmup} warmup steps done")
 
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    total_bytes = 0
-    per_step_bytes = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        b = one_step(events[i])
-        per_step_bytes.append(b)
-        total_bytes += b
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    kern_ms = [s.elapsed_time(e) for s, e in events]
-    launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
+    graph_period = 0
+    if args.graph:
+        graph_period, total_bytes, per_step_bytes, kern_ms, wall = graph_steps(
+            args, w, rip, handles, sched, t, stream, stats)
+        launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
+    else:
+        events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(args.steps)]
+        total_bytes = 0
+        per_step_bytes = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            b = one_step(events[i])
+            per_step_bytes.append(b)
+            total_bytes += b
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        kern_ms = [s.elapsed_time(e) for s, e in events]
+        launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
     err(f"[bench] {args.steps} timed steps: {wall * 1e3:.2f} ms wall")
 
     # host scheduling cost alone (fresh scheduler, same steps)
@@ -318,6 +398,8 @@ def main():
             "host_schedule_us_per_step": round(sched_us, 2),
             "parallelism": "single-gpu",
             "pass": "unfused (local step, then P-Reduce)" if args.unfused else "fused",
+            "launch": (f"hip graph of {graph_period} steps, replayed" if graph_period
+                       else "one library call per step"),
         },
         "roofline": {
             "bound": "hbm",
