@@ -71,17 +71,45 @@ extern "C" int32_t rip_set_max_blocks(int32_t max_blocks) {
 
 namespace {
 
-// Waves per CU at which the fused kernel sustained the most HBM bandwidth on
-// MI355X (measured over workgroup caps of 2-16 waves per CU): more resident
-// waves add outstanding requests without adding bandwidth.  With momentum a
-// lane already keeps three 16-byte loads per member in flight (24 for a group
-// of eight), so those units peak with fewer waves (group of eight: 4 waves
-// 6.09 TB/s, 6 waves 5.99); fp32 and bf16 plain SGD peak at 10.  Odd caps
-// measured the same as the even cap below them (the LDS reservation appears
-// to be granted per half of a CU's LDS), so only even caps are used.
-int target_waves_per_cu(bool bf16, bool mom) {
-  (void)bf16;
-  return mom ? 4 : 10;
+// Resident waves per CU at which each unit shape sustained the most HBM
+// bandwidth on MI355X, by group size k (entry 0: groups above kMaxK, which
+// stream their members in chunks of kMaxK), for units whose members all
+// update (plain SGD, momentum) and for units that only average.  Measured in
+// one process over even caps of 2-16 waves/CU, 32 fp32 replicas of 25.6M
+// parameters, every unit of one size.  A lane keeps 16-byte loads in flight
+// for each slot of each stream it reads (w, plus g and v when the member
+// updates), so units that read more streams peak with fewer resident waves;
+// beyond that, more waves add outstanding requests without adding
+// bandwidth (momentum, GB/s at 4 / 6 / 8 / 10 waves: k = 3 4671 / 5131 /
+// 6019 / 6031, k = 8 6039 / 5960 / 5632 / 5638; averaging only, at 8 / 10 /
+// 12 / 14: k = 2 5561 / 6067 / 6309 / 6382).  Odd caps measured the same as
+// the even cap below them (the LDS reservation appears to be granted per
+// half of a CU's LDS), so only even caps are used.  bf16 units measured like
+// fp32 ones.
+constexpr int kWavesSgd[rip::kMaxK + 1] = {10, 12, 10, 10, 10, 8, 8, 8, 8};
+constexpr int kWavesMom[rip::kMaxK + 1] = {8, 8, 10, 10, 8, 8, 6, 6, 4};
+constexpr int kWavesAvg[rip::kMaxK + 1] = {10, 12, 14, 10, 12, 10, 10, 8, 8};
+
+// Resident waves per CU for one launch: each unit's preference, interpolated
+// by the share of its members that update between the averaging-only and
+// the all-updating shape, averaged over the units weighted by the bytes they
+// move, rounded to an even cap.
+int launch_waves(const rip::StepArgs& a, const int32_t* unit_off, int32_t units,
+                 const uint8_t* is_active, bool mom) {
+  double num = 0.0, den = 0.0;
+  for (int32_t u = 0; u < units; ++u) {
+    const int32_t b = unit_off[u], k = unit_off[u + 1] - b;
+    int32_t act = 0;
+    for (int32_t j = 0; j < k; ++j) act += is_active[a.member[b + j]];
+    const int idx = k <= rip::kMaxK ? k : 0;
+    const double f = (double)act / k;
+    const double pref = f * (mom ? kWavesMom[idx] : kWavesSgd[idx]) + (1.0 - f) * kWavesAvg[idx];
+    const double bytes = act * (mom ? 5.0 : 3.0) + (k - act) * 2.0;
+    num += pref * bytes;
+    den += bytes;
+  }
+  if (den == 0.0) return kWavesSgd[rip::kMaxK];
+  return 2 * (int)(num / den / 2.0 + 0.5);
 }
 
 int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
@@ -325,7 +353,7 @@ namespace {
 // order given, then active workers outside every group, ascending).
 int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const int32_t* members,
                    int32_t n_groups, const int32_t* active, int32_t n_active, const rip_sgd* sgd,
-                   rip::StepArgs& a, bool& mom) {
+                   rip::StepArgs& a, bool& mom, int& waves) {
   const int32_t N = r->n;
   if (n_groups < 0 || n_active < 0) return rip::fail(RIP_E_INVAL, "negative count");
   if (n_groups > 0 && (!group_offsets || !members))
@@ -415,6 +443,7 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
   for (int32_t u = 1; u < units && a.uniform_tiles; ++u)
     if (a.unit_work0[u + 1] - a.unit_work0[u] != a.uniform_tiles) a.uniform_tiles = 0;
   a.flat_numel = r->n_seg == 1 ? r->numel0 : 0;
+  waves = launch_waves(a, unit_off.data(), units, is_active.data(), mom);
   return RIP_OK;
 }
 
@@ -427,7 +456,9 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   if (!r) return rip::fail(RIP_E_INVAL, "rip_preduce: replicas handle is NULL");
   rip::StepArgs a;
   bool mom = false;
-  int32_t rc = build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a, mom);
+  int waves = 0;
+  int32_t rc =
+      build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a, mom, waves);
   if (rc != RIP_OK) return rc;
   if (a.work == 0) return RIP_OK;
   int dev = -1;
@@ -439,7 +470,7 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   const int cap = rip::g_max_blocks.load() > 0 ? rip::g_max_blocks.load() : rip::kDefaultMaxBlocks;
   const int blocks = (int)(a.work < cap ? a.work : cap);
   int bpc = rip::g_blocks_per_cu.load();
-  if (bpc == 0) bpc = target_waves_per_cu(r->dtype == RIP_BF16, mom) * 64 / rip::kBlock;
+  if (bpc == 0) bpc = waves * 64 / rip::kBlock;
   size_t lds = 0;
   if (bpc > 0 && r->lds_per_cu > 0) lds = (size_t)(r->lds_per_cu / bpc) & ~(size_t)255;
   const bool ext = a.wd != 0.0f || a.nesterov != 0;

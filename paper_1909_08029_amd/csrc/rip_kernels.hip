@@ -11,9 +11,10 @@
 // slots x 16 bytes of each member stream; the slot count shrinks as the
 // unit's number of streams grows (see slot_log2), so every lane keeps about
 // 12 16-byte loads in flight whatever the group size (24 for a group of eight
-// with momentum).  The host caps residency at 10 waves per CU, 4 with
-// momentum (an LDS reservation): HBM3E delivered its best rate at that depth
-// of outstanding requests, not at full occupancy.
+// with momentum).  The host caps residency per launch at 4-14 waves per CU
+// (an LDS reservation), fewer when the units read more streams: HBM3E
+// delivered its best rate at a bounded depth of outstanding requests, not at
+// full occupancy.
 // A workgroup handles one unit, so the unit's size k, its member ids and their active
 // flags are wave-uniform: they sit in scalar registers and every branch on
 // them is a scalar branch.  Each thread issues the loads of all members
