@@ -12,25 +12,24 @@ namespace rip {
 #ifndef RIP_BLOCK
 #define RIP_BLOCK 64
 #endif
-#ifndef RIP_LOADS_IN_FLIGHT
-#define RIP_LOADS_IN_FLIGHT 12
-#endif
 constexpr int kBlock = RIP_BLOCK;  // threads per workgroup: one wave64
 constexpr int kMaxK = 8;           // largest group size with a specialized path
 constexpr int kTileOptions = 4;    // tiles of 1, 2, 4 or 8 slots per thread
 
-// A tile of a unit is kBlock threads x 2^slot_log2 slots x 16 bytes of each
-// member stream.  The slot count keeps about RIP_LOADS_IN_FLIGHT 16-byte
-// loads outstanding per thread (k members x w, g and, with momentum, v), so
-// small groups and lone updates still have enough bytes in flight while a
-// workgroup moves a similar number of bytes whatever the group size.  Groups
-// above kMaxK use one slot and stream their members in chunks of kMaxK.
+// A tile of a unit is kBlock threads x 2^slot_log2(k, mom) slots x 16 bytes
+// of each member stream, and a lane keeps one 16-byte load in flight per
+// slot of every stream it reads (w, plus g and v for a member that updates),
+// so small units take several slots: lone updates four, pairs two, groups of
+// three two without momentum and one with it; larger units take one slot,
+// and the host's residency cap sets the depth of outstanding requests.
+// (A group of three without momentum at one slot streamed 2% faster alone,
+// at 14 waves per CU, but the higher cap it needs slowed the mixed-size
+// launches of Global Division by 1%.)  Groups above kMaxK use one slot and
+// stream their members in chunks of kMaxK.
+constexpr int kSlotLog2Sgd[kMaxK + 1] = {0, 2, 1, 1, 0, 0, 0, 0, 0};
+constexpr int kSlotLog2Mom[kMaxK + 1] = {0, 2, 1, 0, 0, 0, 0, 0, 0};
 constexpr int slot_log2(int k, bool mom) {
-  if (k > kMaxK) return 0;
-  const int s = RIP_LOADS_IN_FLIGHT / (k * (mom ? 3 : 2));
-  int l = 0;
-  while (l < kTileOptions - 1 && (2 << l) <= s) ++l;
-  return l;
+  return k > kMaxK ? 0 : (mom ? kSlotLog2Mom[k] : kSlotLog2Sgd[k]);
 }
 
 // Passed by value as the kernel argument (about 2.4 KiB), so each launch

@@ -9,9 +9,8 @@
 // members' buffers, so the launch is a list of (unit, tile) work items, one
 // per single-wave workgroup, unit after unit.  A tile is 64 lanes x 1-8
 // slots x 16 bytes of each member stream; the slot count shrinks as the
-// unit's number of streams grows (see slot_log2), so every lane keeps about
-// 12 16-byte loads in flight whatever the group size (24 for a group of eight
-// with momentum).  The host caps residency per launch at 4-14 waves per CU
+// unit's number of streams grows (see slot_log2), so every lane keeps 8-16
+// 16-byte loads in flight (24 for a group of eight with momentum).  The host caps residency per launch at 4-14 waves per CU
 // (an LDS reservation), fewer when the units read more streams: HBM3E
 // delivered its best rate at a bounded depth of outstanding requests, not at
 // full occupancy.
