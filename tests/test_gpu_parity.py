@@ -117,6 +117,23 @@ def test_segments_with_momentum(dtype, layout):
     check_against_oracle(run, full_windows(w.numel), f"segments {layout}")
 
 
+@pytest.mark.parametrize("dtype,mom", [(DTYPE_F32, 0.9), (DTYPE_BF16, 0.0)])
+def test_many_small_separate_segments(dtype, mom):
+    """Hundreds of separately allocated segments, most shorter than one tile
+    (some empty, some a few elements, a few spanning several tiles): every
+    launch searches a long segment table and most work runs through the
+    element-wise tail path."""
+    rs = np.random.default_rng(33)
+    segs = [int(x) for x in rs.choice([0, 1, 3, 17, 255, 700, 1031, 2048, 9000], size=300)]
+    w = wl.scaled(wl.WORKLOADS[4], segs, steps=5, n=7, dtype=dtype, momentum=mom,
+                  lr=0.1 if dtype == DTYPE_F32 else 20.0,
+                  sched=dict(mode=wl.RANDOM_GB, seed=12, kmin=2, kmax=5))
+    log(f"case many segments: S={len(segs)} P={w.numel} dtype={dtype} mom={mom}")
+    run = DeviceRun(w, "separate")
+    run.run(w.steps)
+    check_against_oracle(run, full_windows(w.numel), "many segments")
+
+
 @pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
 def test_unfused_local_step_then_preduce(dtype):
     """rip_local_step followed by a pure rip_preduce: two stores (for bf16,
