@@ -288,9 +288,12 @@ int32_t rip_step(rip_sched* s, const rip_replicas* r, int64_t step, const uint8_
                  int32_t* group_offsets, int32_t* members, int32_t* n_groups);
 
 /* Launch tuning (process-wide).  rip_set_max_blocks caps the workgroups of
- * one launch (0 = one workgroup per tile); rip_set_blocks_per_cu caps how
- * many of the kernel's workgroups share a compute unit (0 = the library's
- * measured default for the storage type and optimizer). */
+ * one launch (0 = the default: one workgroup per tile up to 2^25
+ * workgroups, beyond which workgroups loop over tiles); rip_set_blocks_per_cu
+ * caps how many of the kernel's workgroups share a compute unit (0 = the
+ * default: chosen per launch from its units' sizes, whether their members
+ * update, and momentum, 4-14 per compute unit).  Negative values are
+ * RIP_E_INVAL.  Results never depend on these settings. */
 int32_t rip_set_max_blocks(int32_t max_blocks);
 int32_t rip_set_blocks_per_cu(int32_t blocks_per_cu);
 
