@@ -8,6 +8,8 @@ segments, and a two-row periodic table of random disjoint groups of any size
 worker 0 eligible one step in three so groups also hold members that do not
 update.  Every element of every replica is compared after a few steps.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -18,7 +20,8 @@ from gpu_util import DeviceRun, check_against_oracle, log
 
 pytestmark = pytest.mark.gpu
 
-CASES = 96
+# RIP_RANDOM_CASES raises the count for a longer one-off run
+CASES = int(os.environ.get("RIP_RANDOM_CASES", "96"))
 
 
 def _random_rows(rs, n, rows=2):
