@@ -32,7 +32,7 @@ constexpr int slot_log2(int k, bool mom) {
   return k > kMaxK ? 0 : (mom ? kSlotLog2Mom[k] : kSlotLog2Sgd[k]);
 }
 
-// Passed by value as the kernel argument (about 2.4 KiB), so each launch
+// Passed by value as the kernel argument (about 2.6 KiB), so each launch
 // carries its own schedule and no device staging buffer is needed.
 struct StepArgs {
   const uint64_t* ptab;       // device [3][S][N]: param, grad, mom pointers
