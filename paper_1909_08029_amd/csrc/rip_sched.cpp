@@ -140,6 +140,10 @@ struct rip_sched {
     std::vector<int32_t> partner;  // ADPSGD: chosen neighbour of a waiting requester
     std::vector<int64_t> seq;      // ADPSGD: request order of a waiting requester
   } st;
+  // The state before the step in progress, kept between steps so that saving
+  // it reuses its allocations instead of making new ones every step.
+  State saved;
+  std::vector<int64_t> ready;  // scratch of schedule_step, kept for its capacity
   std::vector<Row> rows;       // table modes
   std::vector<Group> script;   // SCRIPTED
 
@@ -268,7 +272,7 @@ struct rip_sched {
       for (size_t gi = 0; gi < row.size(); ++gi) {
         if (std::binary_search(row[gi].begin(), row[gi].end(), i)) {
           int64_t key = it * (int64_t)(n + 1) + (int64_t)gi;  // orders as (iteration, gi)
-          st.groups.emplace(key, row[gi]);
+          st.groups.try_emplace(key, row[gi]);  // once per group and iteration
           st.gb[i].push_back(key);
           st.waiting[i] = 1;
           return RIP_OK;
@@ -452,7 +456,8 @@ int32_t schedule_step(rip_sched* s, const uint8_t* eligible, int32_t* active, in
     if (rc != RIP_OK) return rc;
   }
   // Groups whose every member is blocked on them, in id order.
-  std::vector<int64_t> ready;
+  std::vector<int64_t>& ready = s->ready;
+  ready.clear();
   for (int i = 0; i < n; ++i) {
     if (!s->st.waiting[i]) continue;
     const int64_t h = s->st.gb[i].front();
@@ -496,10 +501,14 @@ int32_t schedule_then(rip_sched* s, int64_t step, const uint8_t* eligible, int32
   if (step != s->st.t)
     return fail(RIP_E_INVAL, "steps must be consecutive: expected %lld, got %lld",
                 (long long)s->st.t, (long long)step);
-  rip_sched::State saved = s->st;  // a failed step leaves no trace
+  // A failed step leaves no trace.  Group generation itself can fail only in
+  // the scripted mode (an exhausted or inconsistent script); otherwise only
+  // `then` can, so the state is saved only when one of the two is present.
+  const bool may_fail = then || s->mode == RIP_SCHED_SCRIPTED;
+  if (may_fail) s->saved = s->st;
   int32_t rc = schedule_step(s, eligible, active, n_active, group_offsets, members, n_groups);
   if (rc == RIP_OK && then) rc = then();
-  if (rc != RIP_OK) s->st = std::move(saved);
+  if (rc != RIP_OK && may_fail) s->st = s->saved;
   return rc;
 }
 
