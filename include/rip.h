@@ -52,7 +52,9 @@ enum {
                               group not strictly ascending, duplicate active id,
                               steps not consecutive, exhausted script */
   RIP_E_ALIGN = -2,        /* a device buffer is not 16-byte aligned */
-  RIP_E_OVERLAP = -3,      /* one replica appears in two groups of one call */
+  RIP_E_OVERLAP = -3,      /* one replica appears in two groups of one call,
+                              or a registered buffer that a step writes
+                              overlaps another registered buffer */
   RIP_E_UNSUPPORTED = -4,  /* unknown dtype or mode, or a size above a limit */
   RIP_E_HIP = -5,          /* HIP runtime error (text in rip_last_error) */
   RIP_E_NOMEM = -6         /* host or device allocation failed */
@@ -252,7 +254,8 @@ typedef struct rip_sgd {
 /* Step 2 alone for the `n_active` workers listed in `active` (distinct ids).
  * Same as rip_preduce with no groups.
  * Errors: RIP_E_INVAL (null handle/sgd, ids, no grad or needed mom buffers,
- * Nesterov without momentum). */
+ * Nesterov without momentum, device mismatch), RIP_E_UNSUPPORTED, RIP_E_HIP
+ * as rip_preduce. */
 int32_t rip_local_step(const rip_replicas* r, const int32_t* active, int32_t n_active,
                        const rip_sgd* sgd, void* stream);
 
@@ -262,7 +265,9 @@ int32_t rip_local_step(const rip_replicas* r, const int32_t* active, int32_t n_a
  * .. group_offsets[g+1]-1], strictly ascending).  Groups must be disjoint
  * (RIP_E_OVERLAP otherwise).  sgd == NULL is pure P-Reduce; then n_active
  * must be 0.  One kernel launch covers all groups and updates.
- * Errors: RIP_E_INVAL, RIP_E_OVERLAP, RIP_E_HIP (launch failure). */
+ * Errors: RIP_E_INVAL (also: the current device is not the handle's),
+ * RIP_E_OVERLAP, RIP_E_UNSUPPORTED (a step of 2^31 or more tiles), RIP_E_HIP
+ * (launch failure). */
 int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offsets,
                     const int32_t* members, int32_t n_groups, const int32_t* active,
                     int32_t n_active, const rip_sgd* sgd, void* stream);
