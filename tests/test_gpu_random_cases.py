@@ -20,8 +20,11 @@ from gpu_util import DeviceRun, check_against_oracle, log
 
 pytestmark = pytest.mark.gpu
 
-# RIP_RANDOM_CASES raises the count for a longer one-off run
+# RIP_RANDOM_CASES raises the count for a longer one-off run; RIP_RANDOM_SCALE
+# multiplies the segment sizes and RIP_RANDOM_MAX_N raises the replica count.
 CASES = int(os.environ.get("RIP_RANDOM_CASES", "96"))
+SCALE = int(os.environ.get("RIP_RANDOM_SCALE", "1"))
+MAX_N = int(os.environ.get("RIP_RANDOM_MAX_N", "40"))
 
 
 def _random_rows(rs, n, rows=2):
@@ -42,8 +45,8 @@ def _random_rows(rs, n, rows=2):
 
 def _case(case):
     rs = np.random.default_rng(7000 + case)
-    n = int(rs.integers(1, 41))
-    segs = [int(rs.integers(0, 9000)) for _ in range(int(rs.integers(1, 4)))]
+    n = int(rs.integers(1, MAX_N + 1))
+    segs = [int(rs.integers(0, 9000)) * SCALE for _ in range(int(rs.integers(1, 4)))]
     if rs.random() < 0.3:
         segs.insert(int(rs.integers(0, len(segs) + 1)), 0)
     if sum(segs) == 0:
