@@ -1,7 +1,7 @@
 """Oracle for one step of the P-Reduce algorithm -- test infrastructure only.
 
-What is computed (paper, Sec. 3.2, the algorithm of Fig. 4 "Proposed
-algorithm using P-Reduce"):
+What is computed (paper, Sec. 3.2, and the algorithm of Fig. 4, training
+with P-Reduce):
 
   Step 2 (local update), for every worker i that computes this step:
       x_i <- x_i - eta * grad_i
@@ -26,8 +26,9 @@ operations so that a correct kernel can match it exactly:
               Nesterov u = fl(w - fl(eta*fl(g' + fl(mu*v'))))  -- one rounding
               per operation, never a fused multiply-add;
   * group sum: s = u_{m1}; s = fl(s + u_{mj}) for members in ascending order;
-  * mean:     xbar = fl(s * fl32(1/|G|))  -- the literal "1/|G| times the
-              sum"; fl32(1/k) is the fp32 rounding of the double 1/k;
+  * mean:     xbar = fl(s * fl32(1/|G|))  -- the sum scaled by 1/|G|, as
+              Step 4 writes it; fl32(1/k) is the fp32 rounding of the
+              double 1/k;
   * bf16 storage: widen exactly (bits << 16); round once to nearest-even when
               the step stores (fused form), or after the update and again
               after the average (unfused form: a separate update call followed
