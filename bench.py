@@ -199,6 +199,60 @@ def graph_steps(args, w, rip, handles, sched, t, stream, stats):
     return L, sum(per_step_bytes), per_step_bytes, kern_ms, wall
 
 
+def sweep_caps(args, w, rip, handles, stream):
+    """Kernel GB/s of the workload's steps at each residency cap (resident
+    waves per CU), measured in one process: three rounds, each timing
+    args.steps steps (after two untimed ones) at every cap in turn, each cap
+    with a scheduler of its own.  Prints one JSON line per cap with the
+    median over the rounds."""
+    import torch
+    caps = [int(x) for x in args.sweep_caps.split(",") if x.strip()]
+    if not caps or min(caps) < 1:
+        err("--sweep-caps needs positive waves per CU")
+        sys.exit(2)
+    kw = dict(w.sched)
+    mode = kw.pop("mode")
+    scheds = {c: rip.Scheduler(w.n, mode, **kw) for c in caps}
+    t_next = {c: 0 for c in caps}
+    res = {c: [] for c in caps}
+    for rnd in range(3):
+        for c in caps:
+            rip.rip_set_blocks_per_cu(c)
+            evs, nbytes = [], 0
+            for i in range(args.steps + 2):
+                t = t_next[c]
+                active, groups = rip.rip_schedule_groups(scheds[c], t, w.eligible(t))
+                h = handles[w.grad_slot(t)]
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                if args.average_only:
+                    active = []
+                    rip.rip_preduce(h, groups, [], stream=stream)
+                else:
+                    rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum,
+                                    stream=stream, weight_decay=w.weight_decay,
+                                    nesterov=w.nesterov)
+                e1.record(stream)
+                t_next[c] += 1
+                b = w.alg_bytes(active, groups)
+                if i >= 2 and b:
+                    evs.append((e0, e1))
+                    nbytes += b
+            torch.cuda.synchronize()
+            ms = sum(a.elapsed_time(b) for a, b in evs)
+            res[c].append(nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0)
+        err(f"[bench] sweep round {rnd}: " +
+            "  ".join(f"{c}: {res[c][-1]:.0f}" for c in caps))
+    rip.rip_set_blocks_per_cu(0)
+    for c in caps:
+        print(json.dumps({"sweep": "resident waves per CU", "workload": w.name,
+                          "pass": "average only" if args.average_only else "fused",
+                          "waves_per_cu": c, "gbps_median": round(sorted(res[c])[1], 1),
+                          "gbps_rounds": [round(x, 1) for x in res[c]],
+                          "steps_per_round": args.steps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -221,6 +275,17 @@ def main():
                     help="fixed schedules only (static, rule, table; no straggler): capture "
                          "one period of fused steps into a HIP graph and replay it, so the "
                          "host launches once per period instead of once per step")
+    ap.add_argument("--groups", type=int, default=0,
+                    help="replace the schedule by one table row of consecutive groups of this "
+                         "size, everyone eligible: every unit of one shape")
+    ap.add_argument("--momentum", type=float, default=None,
+                    help="override the workload's momentum")
+    ap.add_argument("--average-only", action="store_true",
+                    help="with --sweep-caps: pure P-Reduce launches, no local update")
+    ap.add_argument("--sweep-caps", default=None,
+                    help="comma-separated resident waves per CU: time --steps steps at each "
+                         "cap in one process, interleaved over three rounds; one JSON line "
+                         "per cap instead of the benchmark line")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM counters)")
     ap.add_argument("--ceiling", action="store_true",
@@ -268,6 +333,14 @@ def main():
         w = wl.scaled(w, w.seg_numel, grad_ring=args.grad_ring)
     if args.schedule:
         w = wl.with_schedule(w, args.schedule)
+    if args.groups:
+        k = args.groups
+        w = wl.scaled(w, w.seg_numel, name=f"{w.name}_groups{k}", straggler_every=None,
+                      sched=dict(mode=wl.TABLE, table=[[tuple(range(i, i + k))
+                                                        for i in range(0, w.n - w.n % k, k)]]))
+    if args.momentum is not None:
+        w = wl.scaled(w, w.seg_numel, name=f"{w.name}_mom{args.momentum:g}",
+                      momentum=args.momentum)
     err(f"[bench] workload {w.name}: N={w.n} P={w.numel} layout={args.layout}")
     if args.max_blocks:
         rip.rip_set_max_blocks(args.max_blocks)
@@ -284,6 +357,9 @@ def main():
 
     stream = torch.cuda.current_stream()
     t = 0
+    if args.sweep_caps:
+        sweep_caps(args, w, rip, handles, stream)
+        return
 
     stats = dict(steps=0, updates=0, groups=0, members=0, empty=0)
 

@@ -75,21 +75,22 @@ namespace {
 // Resident waves per CU at which each unit shape sustained the most HBM
 // bandwidth on MI355X, by group size k (entry 0: groups above kMaxK, which
 // stream their members in chunks of kMaxK), for units whose members all
-// update (plain SGD, momentum) and for units that only average.  Measured in
-// one process over even caps of 2-16 waves/CU, 32 fp32 replicas of 25.6M
-// parameters, every unit of one size.  A lane keeps 16-byte loads in flight
-// for each slot of each stream it reads (w, plus g and v when the member
+// update (plain SGD, momentum) and for units that only average.  Measured
+// with bench.py --sweep-caps (32 fp32 replicas of 25.6M parameters, every
+// unit of one size, even caps of 2-16 waves/CU, one process per shape; two
+// sessions on different machines agreed).  A lane keeps one 16-byte load in
+// flight per slot of every stream it reads (w, plus g and v when the member
 // updates), so units that read more streams peak with fewer resident waves;
-// beyond that, more waves add outstanding requests without adding
-// bandwidth (momentum, GB/s at 4 / 6 / 8 / 10 waves: k = 3 4671 / 5131 /
-// 6019 / 6031, k = 8 6039 / 5960 / 5632 / 5638; averaging only, at 8 / 10 /
-// 12 / 14: k = 2 5561 / 6067 / 6309 / 6382).  Odd caps measured the same as
-// the even cap below them (the LDS reservation appears to be granted per
-// half of a CU's LDS), so only even caps are used.  bf16 units measured like
-// fp32 ones.
-constexpr int kWavesSgd[rip::kMaxK + 1] = {10, 12, 10, 10, 10, 8, 8, 8, 8};
-constexpr int kWavesMom[rip::kMaxK + 1] = {8, 8, 10, 10, 8, 8, 6, 6, 4};
-constexpr int kWavesAvg[rip::kMaxK + 1] = {10, 12, 14, 10, 12, 10, 10, 8, 8};
+// beyond that, more waves add outstanding requests without adding bandwidth
+// (GB/s, plain SGD group of eight at 6 / 8 / 10 waves: 6246 / 5937 / 5892;
+// momentum group of three at 4 / 6 / 8: 4697 / 5154 / 6028).  Where two caps
+// measured within 1%, the table takes the one that also suited the mixed
+// launches of the paper's schedules.  Odd caps measured the same as the even
+// cap below them (the LDS reservation appears to be granted per half of a
+// CU's LDS), so only even caps are used.  bf16 units measured like fp32 ones.
+constexpr int kWavesSgd[rip::kMaxK + 1] = {4, 12, 10, 8, 10, 8, 8, 8, 6};
+constexpr int kWavesMom[rip::kMaxK + 1] = {4, 12, 10, 10, 8, 6, 6, 6, 4};
+constexpr int kWavesAvg[rip::kMaxK + 1] = {6, 12, 14, 10, 12, 10, 8, 8, 8};
 
 // Resident waves per CU for one launch: each unit's preference, interpolated
 // by the share of its members that update between the averaging-only and
