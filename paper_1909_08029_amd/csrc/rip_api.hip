@@ -87,10 +87,12 @@ namespace {
 // measured within 1%, the table takes the one that also suited the mixed
 // launches of the paper's schedules.  Odd caps measured the same as the even
 // cap below them (the LDS reservation appears to be granted per half of a
-// CU's LDS), so only even caps are used.  bf16 units measured like fp32 ones.
+// CU's LDS), so only even caps are used.  bf16 units (8 replicas of 1.3G
+// parameters) peaked at the same caps within 2%, except averaging-only groups
+// of eight, which ran 5% faster at 6 than at 8 (fp32: equal).
 constexpr int kWavesSgd[rip::kMaxK + 1] = {4, 12, 10, 8, 10, 8, 8, 8, 6};
 constexpr int kWavesMom[rip::kMaxK + 1] = {4, 12, 10, 10, 8, 6, 6, 6, 4};
-constexpr int kWavesAvg[rip::kMaxK + 1] = {6, 12, 14, 10, 12, 10, 8, 8, 8};
+constexpr int kWavesAvg[rip::kMaxK + 1] = {6, 12, 14, 10, 12, 10, 8, 8, 6};
 
 // Resident waves per CU for one launch: each unit's preference, interpolated
 // by the share of its members that update between the averaging-only and
