@@ -286,6 +286,9 @@ def main():
                     help="comma-separated resident waves per CU: time --steps steps at each "
                          "cap in one process, interleaved over three rounds; one JSON line "
                          "per cap instead of the benchmark line")
+    ap.add_argument("--native", action="store_true",
+                    help="only run the C-ABI-only program (no Python or torch in the loop) on "
+                         "the workload's shape: configs 1, 2, 3 and 5")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM counters)")
     ap.add_argument("--ceiling", action="store_true",
@@ -307,6 +310,22 @@ def main():
             err("stream_ceiling is not built; run __graft_entry__.build()")
             sys.exit(1)
         sys.exit(subprocess.run([exe] + (["xcd"] if args.ceiling_xcd else [])).returncode)
+
+    if args.native:
+        exe = os.path.join(ROOT, "paper_1909_08029_amd", "rip_bench_native")
+        if not os.path.exists(exe):
+            err("rip_bench_native is not built; run __graft_entry__.build()")
+            sys.exit(1)
+        shapes = {1: ["--replicas", "4", "--params", "1048576", "--fixed", "0,1,2"],
+                  2: ["--replicas", "16", "--params", "25600000", "--group", "4"],
+                  3: ["--replicas", "16", "--params", "138357544", "--group", "8",
+                      "--momentum", "0.9"],
+                  5: ["--replicas", "8", "--params", "1300000000", "--group", "4", "--bf16"]}
+        if args.config not in shapes:
+            err("--native runs the fixed-schedule workloads only (configs 1, 2, 3, 5)")
+            sys.exit(2)
+        sys.exit(subprocess.run([exe, *shapes[args.config], "--steps", str(args.steps),
+                                 "--warmup", str(args.warmup)]).returncode)
 
     import torch
     import paper_1909_08029_amd as rip

@@ -76,11 +76,25 @@ def build_stream_ceiling(out: str = STREAM_CEILING):
     os.replace(tmp, out)
 
 
+NATIVE_BENCH = os.path.join(PKG, "rip_bench_native")
+
+
+def build_native_bench(out: str = NATIVE_BENCH):
+    """The C-ABI-only throughput program run by `bench.py --native`."""
+    tmp = out + ".tmp"
+    _run([HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-Wall",
+          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-I", os.path.join(ROOT, "include"), os.path.join(PKG, "csrc", "rip_bench_native.hip"),
+          "-L", PKG, "-lrip", "-Wl,-rpath,$ORIGIN", "-o", tmp])
+    os.replace(tmp, out)
+
+
 def build_all():
     build_librip()
     build_seedgen()
     build_native_smoke()
     build_stream_ceiling()
+    build_native_bench()
 
 
 if __name__ == "__main__":
