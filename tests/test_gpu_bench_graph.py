@@ -62,3 +62,27 @@ def test_graph_replays_match_oracle(name, w):
             compare(st.window("mom", r, 0, w.numel), vo[r], w.dtype, f"{name} mom r={r}")
     for h in handles:
         h.close()
+
+
+@pytest.mark.parametrize("average_only", [False, True])
+def test_sweep_caps_mode_reports_every_cap(average_only, capsys):
+    """bench.py --sweep-caps runs the steps at each residency cap and prints
+    one JSON line per cap, with the rate of each of its three rounds."""
+    import json
+    import torch
+    import bench
+    import paper_1909_08029_amd as rip
+    torch.cuda.set_device(0)
+    w = CASES[1][1]
+    st = wl.DeviceState(w)
+    st.fill()
+    handles = [rip.Replicas(st.param, gs, st.mom) for gs in st.grad_sets]
+    args = argparse.Namespace(steps=3, sweep_caps="6,10", average_only=average_only)
+    log(f"case sweep caps average_only={average_only}")
+    bench.sweep_caps(args, w, rip, handles, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    lines = [json.loads(l) for l in capsys.readouterr().out.splitlines() if l.startswith("{")]
+    assert [d["waves_per_cu"] for d in lines] == [6, 10]
+    assert all(d["gbps_median"] > 0 and len(d["gbps_rounds"]) == 3 for d in lines)
+    for h in handles:
+        h.close()
