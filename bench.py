@@ -13,7 +13,8 @@ configuration the headline metric is quoted on).
 Prints one JSON line (stdout).  ``value`` is algorithmic HBM bytes of the K
 timed steps divided by their wall time, inputs resident in HBM before timing
 starts.  ``roofline.achieved`` is the algorithmic bytes of one launch over the
-kernel's mean duration measured with HIP events on its stream.
+kernel's mean duration measured with HIP events on its stream, around every
+fifth timed step (``--event-every``).
 ``cpu_baseline`` times the CPU oracle on a bounded sample of the same
 workload.  Progress goes to stderr.
 """
@@ -275,6 +276,9 @@ def main():
                     help="fixed schedules only (static, rule, table; no straggler): capture "
                          "one period of fused steps into a HIP graph and replay it, so the "
                          "host launches once per period instead of once per step")
+    ap.add_argument("--event-every", type=int, default=5,
+                    help="bracket every n-th timed step with HIP events for the kernel's "
+                         "launch duration (1 = every step; each event pair costs wall time)")
     ap.add_argument("--groups", type=int, default=0,
                     help="replace the schedule by one table row of consecutive groups of this "
                          "size, everyone eligible: every unit of one shape")
@@ -382,7 +386,7 @@ def main():
 
     stats = dict(steps=0, updates=0, groups=0, members=0, empty=0)
 
-    def one_step(ev=None):
+    def one_step(ev=None, timed=False):
         nonlocal t
         h = handles[w.grad_slot(t)]
         opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
@@ -399,7 +403,7 @@ def main():
             active, groups = rip.rip_step(sched, h, t, w.lr, eligible=w.eligible(t), **opt)
         if ev is not None:
             ev[1].record(stream)
-        if ev is not None:
+        if timed:
             stats["steps"] += 1
             stats["updates"] += len(active)
             stats["groups"] += sum(1 for g in groups if len(g) > 1)
@@ -421,20 +425,24 @@ def main():
             args, w, rip, handles, sched, t, stream, stats)
         launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
     else:
+        # Every event is a marker packet in the stream; bracketing every step
+        # cost about 1% of the wall-clock rate, so only every n-th step is
+        # bracketed (its launch duration is the kernel's, as before).
+        every = max(1, args.event_every)
         events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(args.steps)]
+                  if i % every == 0 else None for i in range(args.steps)]
         total_bytes = 0
         per_step_bytes = []
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(args.steps):
-            b = one_step(events[i])
+            b = one_step(events[i], timed=True)
             per_step_bytes.append(b)
             total_bytes += b
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        kern_ms = [s.elapsed_time(e) for s, e in events]
-        launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
+        launched = [(b, ev[0].elapsed_time(ev[1])) for b, ev in zip(per_step_bytes, events)
+                    if ev is not None and b > 0]
     err(f"[bench] {args.steps} timed steps: {wall * 1e3:.2f} ms wall")
 
     # host scheduling cost alone (fresh scheduler, same steps)
@@ -507,6 +515,7 @@ def main():
             "mean_kernel_us": round(mean_kernel_ms * 1e3, 2),
             "median_kernel_us": round(median_kernel_ms * 1e3, 2),
             "launches_timed": len(launched),
+            "timed_every_nth_step": 1 if graph_period else max(1, args.event_every),
         },
         "cpu_baseline": cpu,
     }
