@@ -26,9 +26,11 @@ def test_scheduler_fuzz_under_sanitizers():
                "-o", exe]
         build = subprocess.run(cmd, capture_output=True, text=True, timeout=300)
         assert build.returncode == 0, build.stderr[-3000:]
-        env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=0",
+        # The process environment is passed on unchanged; ASan is told not to
+        # insist on being the first library loaded.
+        env = dict(os.environ,
+                   ASAN_OPTIONS="detect_leaks=1:abort_on_error=0:verify_asan_link_order=0",
                    UBSAN_OPTIONS="print_stacktrace=1")
-        env.pop("LD_PRELOAD", None)
         res = subprocess.run([exe, "3000"], capture_output=True, text=True, timeout=600, env=env)
         assert res.returncode == 0, (res.stdout[-2000:], res.stderr[-4000:])
         assert "sched fuzz ok" in res.stdout
