@@ -35,7 +35,8 @@ HBM_PEAK_GBPS = 8000.0
 METRIC = "P-Reduce+update effective HBM GB/s and % of MI355X HBM peak"
 KERNEL_SOURCES = ["paper_1909_08029_amd/csrc/rip_kernels.hip",
                   "paper_1909_08029_amd/csrc/rip_api.hip",
-                  "paper_1909_08029_amd/csrc/rip_kernel_args.h"]
+                  "paper_1909_08029_amd/csrc/rip_kernel_args.h",
+                  "paper_1909_08029_amd/csrc/rip_launch_policy.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 SCHEDULE_NAMES = ["table", "static", "random_gb", "global_division", "scripted", "rule",
                   "inter_intra", "adpsgd"]

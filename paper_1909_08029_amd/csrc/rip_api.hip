@@ -5,7 +5,6 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cmath>
 #include <atomic>
 #include <cstdarg>
 #include <cstdio>
@@ -16,6 +15,7 @@
 
 #include "rip_internal.h"
 #include "rip_kernel_args.h"
+#include "rip_launch_policy.h"
 
 namespace rip {
 
@@ -72,52 +72,7 @@ extern "C" int32_t rip_set_max_blocks(int32_t max_blocks) {
 
 namespace {
 
-// Resident waves per CU at which each unit shape sustained the most HBM
-// bandwidth on MI355X, by group size k (entry 0: groups above kMaxK, which
-// stream their members in chunks of kMaxK), for units whose members all
-// update (plain SGD, momentum) and for units that only average.  Measured
-// with bench.py --sweep-caps (32 fp32 replicas of 25.6M parameters, every
-// unit of one size, even caps of 2-16 waves/CU, one process per shape; two
-// sessions on different machines agreed).  A lane keeps one 16-byte load in
-// flight per slot of every stream it reads (w, plus g and v when the member
-// updates), so units that read more streams peak with fewer resident waves;
-// beyond that, more waves add outstanding requests without adding bandwidth
-// (GB/s, plain SGD group of eight at 6 / 8 / 10 waves: 6246 / 5937 / 5892;
-// momentum group of three at 4 / 6 / 8: 4697 / 5154 / 6028).  Where two caps
-// measured within 1%, the table takes the one that also suited the mixed
-// launches of the paper's schedules.  Odd caps measured the same as the even
-// cap below them (the LDS reservation appears to be granted per half of a
-// CU's LDS), so only even caps are used.  bf16 units (8 replicas of 1.3G
-// parameters) peaked at the same caps within 2%, except averaging-only groups
-// of eight, which ran 5% faster at 6 than at 8 (fp32: equal).
-constexpr int kWavesSgd[rip::kMaxK + 1] = {4, 12, 10, 8, 10, 8, 8, 8, 6};
-constexpr int kWavesMom[rip::kMaxK + 1] = {4, 12, 10, 10, 8, 6, 6, 6, 4};
-constexpr int kWavesAvg[rip::kMaxK + 1] = {6, 12, 14, 10, 12, 10, 8, 8, 6};
-
-// Resident waves per CU for one launch: each unit's preference, interpolated
-// by the share of its members that update between the averaging-only and
-// the all-updating shape, averaged over the units weighted by the bytes they
-// move.
-int launch_waves(const rip::StepArgs& a, const int32_t* unit_off, int32_t units,
-                 const uint8_t* is_active, bool mom) {
-  double num = 0.0, den = 0.0;
-  for (int32_t u = 0; u < units; ++u) {
-    const int32_t b = unit_off[u], k = unit_off[u + 1] - b;
-    int32_t act = 0;
-    for (int32_t j = 0; j < k; ++j) act += is_active[a.member[b + j]];
-    const int idx = k <= rip::kMaxK ? k : 0;
-    const double f = (double)act / k;
-    const double pref = f * (mom ? kWavesMom[idx] : kWavesSgd[idx]) + (1.0 - f) * kWavesAvg[idx];
-    const double bytes = act * (mom ? 5.0 : 3.0) + (k - act) * 2.0;
-    num += pref * bytes;
-    den += bytes;
-  }
-  if (den == 0.0) return kWavesSgd[rip::kMaxK];
-  // Round up to an even cap: a cap below a shape's preference cost more
-  // (SGD groups of 2-4 at 8 waves: -3%) than one above it (groups of 5-8 at
-  // 10: -1%).
-  return 2 * (int)std::ceil(num / den / 2.0 - 1e-6);
-}
+static_assert(rip::policy::kMaxK == rip::kMaxK, "launch policy and kernel disagree on kMaxK");
 
 int elems_per_16b(int32_t dtype) { return dtype == RIP_BF16 ? 8 : 4; }
 int elem_size(int32_t dtype) { return dtype == RIP_BF16 ? 2 : 4; }
@@ -450,7 +405,14 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
   for (int32_t u = 1; u < units && a.uniform_tiles; ++u)
     if (a.unit_work0[u + 1] - a.unit_work0[u] != a.uniform_tiles) a.uniform_tiles = 0;
   a.flat_numel = r->n_seg == 1 ? r->numel0 : 0;
-  waves = launch_waves(a, unit_off.data(), units, is_active.data(), mom);
+  int32_t unit_k[RIP_MAX_REPLICAS], unit_act[RIP_MAX_REPLICAS];
+  for (int32_t u = 0; u < units; ++u) {
+    const int32_t b = unit_off[u];
+    unit_k[u] = unit_off[u + 1] - b;
+    unit_act[u] = 0;
+    for (int32_t j = 0; j < unit_k[u]; ++j) unit_act[u] += is_active[a.member[b + j]];
+  }
+  waves = rip::policy::launch_waves(unit_k, unit_act, units, mom);
   return RIP_OK;
 }
 
