@@ -6,17 +6,19 @@
 A step is one pass of the whole hot path over one batch of synthetic input:
 the host group schedule for step t, then one launch of the fused kernel that
 applies every active worker's local update and the P-Reduce of every group.
-The default workload is 16 fp32 replicas of a 25.6M-parameter (ResNet-50
-sized) model with a seeded static schedule of four groups of four (the
-configuration the headline metric is quoted on).
+The default workload (--config 5) is the largest of the five: 8 replicas of
+1.3 B parameters stored as bf16 (fp32 arithmetic), a seeded static schedule
+of two groups of four, plain SGD.  --config 1..4 select the others.
 
 Prints one JSON line (stdout).  ``value`` is algorithmic HBM bytes of the K
 timed steps divided by their wall time, inputs resident in HBM before timing
-starts.  ``roofline.achieved`` is the algorithmic bytes of one launch over the
-kernel's mean duration measured with HIP events on its stream, around every
-fifth timed step (``--event-every``).
-``cpu_baseline`` times the CPU oracle on a bounded sample of the same
-workload.  Progress goes to stderr.
+starts.  ``roofline.achieved`` is the same bytes over the GPU time of the
+timed launches: one pair of HIP events on the launch stream brackets the
+whole timed window, and the span is spread evenly over the launches in it
+(the next launch is queued before the previous kernel ends, so the span is
+kernel time plus the dispatch gaps between launches; it can never exceed the
+wall time).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
+same workload, pinned to one core.  Progress goes to stderr.
 """
 from __future__ import annotations
 
@@ -97,10 +99,14 @@ def host_cpu() -> str:
 
 
 def cpu_baseline(w, seconds: float = 12.0):
-    """The oracle as it stands, single-threaded numpy, on one window of every
-    replica, for as many steps of the workload's schedule as fit the budget
-    (at least 2).  Times the update + group averaging only."""
-    import numpy as np
+    """The oracle as it stands (numpy) on one window of every replica, for as
+    many steps of the workload's schedule as fit the budget (at least 2),
+    timed on the update + group averaging only.  It runs on one core: the
+    calling thread is pinned to one CPU and numpy's thread pools are limited
+    to one thread for the duration (numpy's element-wise operations are
+    single-threaded anyway)."""
+    import numpy as np  # noqa: F401
+    from threadpoolctl import threadpool_limits
     from oracle import preduce as op
     from oracle import sched as osd
     from seedgen import DTYPE_BF16
@@ -115,20 +121,27 @@ def cpu_baseline(w, seconds: float = 12.0):
     dt = op.BF16 if w.dtype == DTYPE_BF16 else op.F32
     sub = wl.scaled(w, [width])
     spent, nbytes, steps = 0.0, 0, 0
-    while steps < 2 or (spent < seconds and steps < w.steps):
-        active, groups = sch.step(steps, w.eligible(steps))
-        g = grad(w.grad_slot(steps))
-        t0 = time.perf_counter()
-        p, v = op.step(p, g, v, groups, active, w.lr, w.momentum or None, dt, True,
-                       w.weight_decay, w.nesterov)
-        spent += time.perf_counter() - t0
-        nbytes += sub.alg_bytes(active, groups)
-        steps += 1
+    before = os.sched_getaffinity(0)
+    cpu = min(before)
+    os.sched_setaffinity(0, {cpu})           # this thread only
+    try:
+        with threadpool_limits(limits=1):
+            while steps < 2 or (spent < seconds and steps < w.steps):
+                active, groups = sch.step(steps, w.eligible(steps))
+                g = grad(w.grad_slot(steps))
+                t0 = time.perf_counter()
+                p, v = op.step(p, g, v, groups, active, w.lr, w.momentum or None, dt, True,
+                               w.weight_decay, w.nesterov)
+                spent += time.perf_counter() - t0
+                nbytes += sub.alg_bytes(active, groups)
+                steps += 1
+    finally:
+        os.sched_setaffinity(0, before)
     return dict(value=round(nbytes / spent / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
                 sample=f"{steps} steps of the workload schedule on elements [0, {width}) of all "
-                       f"{w.n} replicas ({100.0 * width / w.numel:.1f}% of each replica), "
-                       f"numpy single-threaded on {host_cpu()}; "
-                       f"{spent:.1f} s timed, update+average only")
+                       f"{w.n} replicas ({100.0 * width / w.numel:.2f}% of each replica), "
+                       f"numpy pinned to CPU {cpu} with thread pools limited to 1, on "
+                       f"{host_cpu()}; {spent:.1f} s timed, update+average only")
 
 
 def graph_steps(args, w, rip, handles, sched, t, stream, stats):
@@ -138,8 +151,8 @@ def graph_steps(args, w, rip, handles, sched, t, stream, stats):
     (a multiple of the gradient ring) are scheduled by the library, their
     launches captured into a HIP graph, and a second scheduler checks that the
     next period schedules exactly the same groups.  Every replay then runs
-    those steps, as a static schedule prescribes.  Returns (period, total
-    bytes, bytes per step, kernel ms per step, wall seconds)."""
+    those steps, as a static schedule prescribes.  Returns (period,
+    bytes per step, GPU span in ms of all replays, wall seconds)."""
     import math
     import torch
     from seedgen import workloads as wl
@@ -176,29 +189,28 @@ def graph_steps(args, w, rip, handles, sched, t, stream, stats):
     torch.cuda.synchronize()
     step_bytes = [w.alg_bytes(a, gr) for a, gr in period]
     reps = args.steps // L
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(reps)]
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for e0, e1 in events:
-        e0.record(stream)
+    e0.record(stream)
+    for _ in range(reps):
         g.replay()
-        e1.record(stream)
+    e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_step_bytes, kern_ms = [], []
-    for e0, e1 in events:
-        ms = e0.elapsed_time(e1) / L               # graph time spread over its launches
+    span_ms = e0.elapsed_time(e1)
+    per_step_bytes = []
+    for _ in range(reps):
         for (active, groups), b in zip(period, step_bytes):
             per_step_bytes.append(b)
-            kern_ms.append(ms)
             stats["steps"] += 1
             stats["updates"] += len(active)
             stats["groups"] += sum(1 for x in groups if len(x) > 1)
             stats["members"] += sum(len(x) for x in groups if len(x) > 1)
             stats["empty"] += 0 if (active or any(len(x) > 1 for x in groups)) else 1
     del g
-    return L, sum(per_step_bytes), per_step_bytes, kern_ms, wall
+    return L, per_step_bytes, span_ms, wall
 
 
 def sweep_caps(args, w, rip, handles, stream):
@@ -255,12 +267,25 @@ def sweep_caps(args, w, rip, handles, stream):
                           "steps_per_round": args.steps}), flush=True)
 
 
+def run_program(name, argv):
+    """Builds one of the measurement programs beside bench.py (before any GPU
+    work in this process) and runs it as a child process."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location(
+        "rip_build", os.path.join(ROOT, "paper_1909_08029_amd", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    exe = mod.build_bench_program(name)
+    sys.exit(subprocess.run([exe, *argv]).returncode)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5],
+                    help="workload (default 5, the largest: 8 x 1.3B bf16, two groups of four)")
     ap.add_argument("--layout", default="flat", choices=["flat", "separate"])
     ap.add_argument("--grad-ring", type=int, default=None)
     ap.add_argument("--schedule", default=None,
@@ -277,9 +302,6 @@ def main():
                     help="fixed schedules only (static, rule, table; no straggler): capture "
                          "one period of fused steps into a HIP graph and replay it, so the "
                          "host launches once per period instead of once per step")
-    ap.add_argument("--event-every", type=int, default=5,
-                    help="bracket every n-th timed step with HIP events for the kernel's "
-                         "launch duration (1 = every step; each event pair costs wall time)")
     ap.add_argument("--groups", type=int, default=0,
                     help="replace the schedule by one table row of consecutive groups of this "
                          "size, everyone eligible: every unit of one shape")
@@ -292,14 +314,13 @@ def main():
                          "cap in one process, interleaved over three rounds; one JSON line "
                          "per cap instead of the benchmark line")
     ap.add_argument("--native", action="store_true",
-                    help="only run the C-ABI-only program (no Python or torch in the loop) on "
-                         "the workload's shape: configs 1, 2, 3 and 5")
+                    help="only run bench_native.hip (the C ABI from a C++ loop, no Python or "
+                         "torch) on the workload's shape: configs 1, 2, 3 and 5")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM counters)")
     ap.add_argument("--ceiling", action="store_true",
-                    help="only run the bare-stream HBM ceiling program (random vs zero data)")
-    ap.add_argument("--ceiling-xcd", action="store_true",
-                    help="only run the ceiling program's XCD tile-placement sweep")
+                    help="only run bench_ceiling.hip, bare HBM streams of the kernel's access "
+                         "shapes (random vs zero data)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -309,18 +330,10 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    if args.ceiling or args.ceiling_xcd:
-        exe = os.path.join(ROOT, "paper_1909_08029_amd", "stream_ceiling")
-        if not os.path.exists(exe):
-            err("stream_ceiling is not built; run __graft_entry__.build()")
-            sys.exit(1)
-        sys.exit(subprocess.run([exe] + (["xcd"] if args.ceiling_xcd else [])).returncode)
+    if args.ceiling:
+        run_program("bench_ceiling", [])
 
     if args.native:
-        exe = os.path.join(ROOT, "paper_1909_08029_amd", "rip_bench_native")
-        if not os.path.exists(exe):
-            err("rip_bench_native is not built; run __graft_entry__.build()")
-            sys.exit(1)
         shapes = {1: ["--replicas", "4", "--params", "1048576", "--fixed", "0,1,2"],
                   2: ["--replicas", "16", "--params", "25600000", "--group", "4"],
                   3: ["--replicas", "16", "--params", "138357544", "--group", "8",
@@ -329,8 +342,8 @@ def main():
         if args.config not in shapes:
             err("--native runs the fixed-schedule workloads only (configs 1, 2, 3, 5)")
             sys.exit(2)
-        sys.exit(subprocess.run([exe, *shapes[args.config], "--steps", str(args.steps),
-                                 "--warmup", str(args.warmup)]).returncode)
+        run_program("bench_native", [*shapes[args.config], "--steps", str(args.steps),
+                                     "--warmup", str(args.warmup)])
 
     import torch
     import paper_1909_08029_amd as rip
@@ -387,23 +400,22 @@ def main():
 
     stats = dict(steps=0, updates=0, groups=0, members=0, empty=0)
 
-    def one_step(ev=None, timed=False):
+    def one_step(timed=False):
+        """One step; returns (algorithmic bytes, kernel launches)."""
         nonlocal t
         h = handles[w.grad_slot(t)]
         opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
                    nesterov=w.nesterov)
-        if ev is not None:
-            ev[0].record(stream)
         if args.unfused:
             active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
             if active:
                 rip.rip_local_step(h, active, w.lr, **opt)
             rip.rip_preduce(h, groups, stream=stream)
+            launches = int(bool(active)) + int(any(len(g) > 1 for g in groups))
         else:
             # group generation and the fused launch in one library call
             active, groups = rip.rip_step(sched, h, t, w.lr, eligible=w.eligible(t), **opt)
-        if ev is not None:
-            ev[1].record(stream)
+            launches = int(bool(active) or any(len(g) > 1 for g in groups))
         if timed:
             stats["steps"] += 1
             stats["updates"] += len(active)
@@ -412,8 +424,8 @@ def main():
             stats["empty"] += 0 if (active or any(len(g) > 1 for g in groups)) else 1
         t += 1
         if args.unfused:
-            return w.alg_bytes_unfused(active, groups)
-        return w.alg_bytes(active, groups)
+            return w.alg_bytes_unfused(active, groups), launches
+        return w.alg_bytes(active, groups), launches
 
     for _ in range(args.warmup):
         one_step()
@@ -422,29 +434,29 @@ def main():
 
     graph_period = 0
     if args.graph:
-        graph_period, total_bytes, per_step_bytes, kern_ms, wall = graph_steps(
+        graph_period, per_step_bytes, span_ms, wall = graph_steps(
             args, w, rip, handles, sched, t, stream, stats)
-        launched = [(b, ms) for b, ms in zip(per_step_bytes, kern_ms) if b > 0]
+        total_bytes = sum(per_step_bytes)
+        launches = sum(1 for b in per_step_bytes if b > 0)
     else:
-        # Every event is a marker packet in the stream; bracketing every step
-        # cost about 1% of the wall-clock rate, so only every n-th step is
-        # bracketed (its launch duration is the kernel's, as before).
-        every = max(1, args.event_every)
-        events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  if i % every == 0 else None for i in range(args.steps)]
-        total_bytes = 0
-        per_step_bytes = []
+        # One event pair brackets the whole timed window on the launch
+        # stream: markers between steps would add packets to the stream.
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        total_bytes, launches = 0, 0
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        e0.record(stream)
         for i in range(args.steps):
-            b = one_step(events[i], timed=True)
-            per_step_bytes.append(b)
+            b, n_launch = one_step(timed=True)
             total_bytes += b
+            launches += n_launch
+        e1.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        launched = [(b, ev[0].elapsed_time(ev[1])) for b, ev in zip(per_step_bytes, events)
-                    if ev is not None and b > 0]
-    err(f"[bench] {args.steps} timed steps: {wall * 1e3:.2f} ms wall")
+        span_ms = e0.elapsed_time(e1)
+    err(f"[bench] {args.steps} timed steps: {wall * 1e3:.2f} ms wall, "
+        f"{span_ms:.2f} ms GPU span, {launches} launches")
 
     # host scheduling cost alone (fresh scheduler, same steps)
     sched_kw = dict(w.sched)
@@ -455,10 +467,9 @@ def main():
     sched_us = (time.perf_counter() - h0) / args.steps * 1e6
 
     value = total_bytes / wall / 1e9
-    mean_launch_bytes = sum(b for b, _ in launched) / max(1, len(launched))
-    mean_kernel_ms = sum(ms for _, ms in launched) / max(1, len(launched))
-    median_kernel_ms = sorted(ms for _, ms in launched)[len(launched) // 2] if launched else 0.0
-    achieved = mean_launch_bytes / (mean_kernel_ms * 1e-3) / 1e9 if launched else 0.0
+    mean_launch_bytes = total_bytes / max(1, launches)
+    mean_kernel_ms = span_ms / max(1, launches)
+    achieved = total_bytes / (span_ms * 1e-3) / 1e9 if span_ms > 0 else 0.0
     traffic = None
     if args.layout == "flat" and not args.grad_ring and not args.unfused:
         traffic = load_traffic(w.name, mean_launch_bytes)
@@ -479,6 +490,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
+        # the arithmetic type: every value is computed in fp32, whatever the
+        # storage type (config.storage)
         "dtype": "f32",
         "data": "synthetic",
         "config": {
@@ -512,11 +525,11 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
-            "alg_bytes_per_launch": int(mean_launch_bytes),
+            "alg_bytes_per_launch": int(round(mean_launch_bytes)),
             "mean_kernel_us": round(mean_kernel_ms * 1e3, 2),
-            "median_kernel_us": round(median_kernel_ms * 1e3, 2),
-            "launches_timed": len(launched),
-            "timed_every_nth_step": 1 if graph_period else max(1, args.event_every),
+            "launches_timed": launches,
+            "kernel_time": "GPU span of the timed window (one HIP event pair on the launch "
+                           "stream) / launches in it",
         },
         "cpu_baseline": cpu,
     }

@@ -23,19 +23,10 @@
 // sustained bandwidth depends on the data moved.  Standalone program; prints
 // one line per (data, waves/CU) with GB/s counted as bytes the stream moves
 // divided by kernel time (5 back-to-back launches after one warm-up).
-//
-// With the argument "xcd" it instead measures XCD-aware tile placement:
-// it prints the XCD (hardware XCC_ID register) each of the first 64
-// workgroups runs on, then times the read, copy and group4-global streams with the
-// tiles permuted over workgroups so that XCD x (workgroup b runs on XCD
-// b mod 8) handles the tiles whose chunk index (tile / C) is congruent to
-// x + s mod 8, for chunk sizes C of 1 to 2048 tiles, or a contiguous eighth
-// of every stream per XCD.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 #include <cstdio>
-#include <cstring>
 
 namespace {
 
@@ -56,19 +47,7 @@ struct Streams {
   char* p[kStreams];
   uint32_t tiles;  // workgroups; each covers kLanes x 16 bytes of every stream it touches
   float lr;
-  // Tile placement: mode 0 = tile b on workgroup b; mode 1 = chunks of
-  // `chunk` tiles dealt to XCDs (shifted by `shift`); mode 2 = one
-  // contiguous eighth per XCD.  Every mode is a bijection on [0, grid).
-  int mode;
-  uint32_t chunk, shift;
 };
-
-__device__ __forceinline__ uint32_t place(const Streams& s, uint32_t b, uint32_t grid) {
-  const uint32_t x = b & 7, i = b >> 3;
-  if (s.mode == 1) return ((i / s.chunk) * 8 + ((x + s.shift) & 7)) * s.chunk + i % s.chunk;
-  if (s.mode == 2) return ((x + s.shift) & 7) * (grid >> 3) + i;
-  return b;
-}
 
 enum Kind { kRead = 0, kCopy = 1, k2R1W = 2, kGroup4 = 3, kGroup8Mom = 4, kGroup4Buf = 5,
             kGroup8MomBuf = 6 };
@@ -94,8 +73,7 @@ __device__ __forceinline__ void bstore(Rsrc r, f32x4 v) {
 template <int KIND>
 __global__ __launch_bounds__(kLanes) void stream_kernel(Streams s) {
   const uint32_t grid = KIND == kRead ? s.tiles / 4 : s.tiles;
-  if (blockIdx.x >= grid) return;
-  const uint32_t t = place(s, blockIdx.x, grid);
+  const uint32_t t = blockIdx.x;
   if (t >= grid) return;
   if constexpr (KIND == kRead) {
     // 4 tiles per workgroup so each lane keeps 4 loads in flight
@@ -187,13 +165,6 @@ __global__ __launch_bounds__(kLanes) void stream_kernel(Streams s) {
   }
 }
 
-// The XCD each workgroup runs on (XCC_ID hardware register, bits 3:0).
-__global__ void xcc_of_workgroup(uint32_t* out, uint32_t n) {
-  uint32_t v;
-  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
-  if (blockIdx.x < n && threadIdx.x == 0) out[blockIdx.x] = v & 0xFu;
-}
-
 // Uniform values in [-scale, scale) from a SplitMix64-style hash of the index.
 __global__ void fill_random(float* p, int64_t n, uint64_t seed, float scale) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -238,48 +209,7 @@ double time_ms(const Streams& s, size_t lds_bytes) {
 
 }  // namespace
 
-int xcd_sweep(Streams s, int lds_per_cu, double gb) {
-  uint32_t* d = nullptr;
-  uint32_t h[64];
-  if (hipMalloc(&d, sizeof h) != hipSuccess) return 1;
-  hipLaunchKernelGGL(xcc_of_workgroup, dim3(64), dim3(kLanes), 0, 0, d, 64u);
-  if (hipMemcpy(h, d, sizeof h, hipMemcpyDeviceToHost) != hipSuccess) return 1;
-  (void)hipFree(d);
-  std::printf("XCD of workgroups 0..63:");
-  for (uint32_t v : h) std::printf(" %u", v);
-  std::printf("\n");
-  struct Place { int mode; uint32_t chunk, shift; };
-  Place ps[32];
-  int n = 0;
-  ps[n++] = {0, 1, 0};
-  for (uint32_t c : {1u, 4u, 16u, 64u, 256u, 2048u})
-    for (uint32_t sh : {0u, 1u, 2u, 4u})
-      if (!(c == 1 && sh == 0)) ps[n++] = {1, c, sh};
-  ps[n++] = {2, 1, 0};
-  ps[n++] = {2, 1, 4};
-  for (int waves : {10, 0}) {
-    const size_t lds = waves ? ((size_t)(lds_per_cu / waves) & ~(size_t)255) : 0;
-    for (int i = 0; i < n; ++i) {
-      Streams x = s;
-      x.mode = ps[i].mode;
-      x.chunk = ps[i].chunk;
-      x.shift = ps[i].shift;
-      const double t_read = time_ms<kRead>(x, lds), t_copy = time_ms<kCopy>(x, lds);
-      const double t_g4 = time_ms<kGroup4>(x, lds);
-      if (t_read < 0 || t_copy < 0 || t_g4 < 0) return 1;
-      std::printf("waves/CU=%-3s placement=%s chunk=%-4u shift=%u  read %7.1f  copy %7.1f  "
-                  "group4-global %7.1f GB/s\n",
-                  waves ? "10" : "max",
-                  x.mode == 0 ? "identity" : (x.mode == 1 ? "chunks  " : "eighths "), x.chunk,
-                  x.shift, gb / t_read * 1e3, 2 * gb / t_copy * 1e3, 12 * gb / t_g4 * 1e3);
-      std::fflush(stdout);
-    }
-  }
-  return 0;
-}
-
-int main(int argc, char** argv) {
-  const bool xcd = argc > 1 && std::strcmp(argv[1], "xcd") == 0;
+int main() {
   const int64_t bytes = 1ll << 30;  // per stream
   Streams s{};
   for (int j = 0; j < kStreams; ++j)
@@ -298,15 +228,6 @@ int main(int argc, char** argv) {
   std::printf("stream ceilings on %s, %d CUs, 1 GiB per stream, non-temporal 16-byte accesses\n",
               prop.gcnArchName, cus);
   const double gb = (double)bytes / 1e9;
-  if (xcd) {
-    for (int j = 0; j < kStreams; ++j)
-      hipLaunchKernelGGL(fill_random, dim3(8192), dim3(256), 0, 0, reinterpret_cast<float*>(s.p[j]),
-                         bytes / 4, (uint64_t)(1000 + j), j < 4 ? 1.0f : 0.01f);
-    if (hipDeviceSynchronize() != hipSuccess) return 1;
-    const int rc = xcd_sweep(s, lds_per_cu, gb);
-    for (int j = 0; j < kStreams; ++j) (void)hipFree(s.p[j]);
-    return rc;
-  }
   for (int random = 1; random >= 0; --random) {
     for (int j = 0; j < kStreams; ++j) {
       if (random) {

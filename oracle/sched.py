@@ -62,6 +62,32 @@ MAX_STATIC_ATTEMPTS = 1000
 
 
 # ---------------------------------------------------------------------------
+# seeded draws
+# ---------------------------------------------------------------------------
+def shuffle(items: list, rng: Stream) -> list:
+    """Fisher-Yates (Knuth's Algorithm P, drawn from the last position down):
+    position a = L-1 .. 1 swaps with position rng.bounded(a + 1) in [0, a].
+    Every permutation comes from exactly one draw sequence.  In place;
+    returns the list."""
+    for a in range(len(items) - 1, 0, -1):
+        b = rng.bounded(a + 1)
+        items[a], items[b] = items[b], items[a]
+    return items
+
+
+def partial_shuffle(items: list, m: int, rng: Stream) -> list:
+    """The first m steps of Fisher-Yates drawn from the front: position
+    j = 0 .. m-1 swaps with position j + rng.bounded(L - j) in [j, L).  The
+    first m items are then a uniform ordered selection; every ordered
+    selection comes from exactly one draw sequence.  In place; returns the
+    list."""
+    for j in range(m):
+        x = j + rng.bounded(len(items) - j)
+        items[j], items[x] = items[x], items[j]
+    return items
+
+
+# ---------------------------------------------------------------------------
 # periodic tables
 # ---------------------------------------------------------------------------
 def union_connected(n: int, rows: Sequence[Sequence[Sequence[int]]]) -> bool:
@@ -93,11 +119,7 @@ def static_table(n: int, k: int, period: int, seed: int) -> List[List[Tuple[int,
     for attempt in range(MAX_STATIC_ATTEMPTS):
         rows = []
         for rho in range(period):
-            s = Stream(fold(seed, SCHED_TAG, attempt, rho))
-            a = list(range(n))
-            for i in range(n - 1, 0, -1):
-                j = s.bounded(i + 1)
-                a[i], a[j] = a[j], a[i]
+            a = shuffle(list(range(n)), Stream(fold(seed, SCHED_TAG, attempt, rho)))
             groups = [tuple(sorted(a[c:c + k])) for c in range(0, n, k)]
             groups.sort(key=lambda g: g[0])
             rows.append(groups)
@@ -201,18 +223,13 @@ class Scheduler:
     def _random_group(self, i: int):
         n = self.n
         k = min(self.kmin + self.rng.bounded(self.kmax - self.kmin + 1), n)
-        others = [j for j in range(n) if j != i]
-        for j in range(k - 1):
-            x = j + self.rng.bounded(n - 1 - j)
-            others[j], others[x] = others[x], others[j]
+        others = partial_shuffle([j for j in range(n) if j != i], k - 1, self.rng)
         self._new_group([i] + others[:k - 1])
 
     def _global_division(self, i: int):
         idle = [w for w in range(self.n) if not self.gb[w] and
                 (self.c_thres <= 0 or self.c[i] - self.c[w] < self.c_thres)]
-        for a in range(len(idle) - 1, 0, -1):
-            b = self.rng.bounded(a + 1)
-            idle[a], idle[b] = idle[b], idle[a]
+        shuffle(idle, self.rng)
         pos, made = 0, []
         while pos < len(idle):
             k = self.kmin + self.rng.bounded(self.kmax - self.kmin + 1)
@@ -222,10 +239,7 @@ class Scheduler:
 
     def _chunks(self, members):
         """Fisher-Yates shuffle, then consecutive chunks of drawn sizes."""
-        members = list(members)
-        for a in range(len(members) - 1, 0, -1):
-            b = self.rng.bounded(a + 1)
-            members[a], members[b] = members[b], members[a]
+        members = shuffle(list(members), self.rng)
         pos, out = 0, []
         while pos < len(members):
             k = self.kmin + self.rng.bounded(self.kmax - self.kmin + 1)

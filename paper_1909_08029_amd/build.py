@@ -65,36 +65,33 @@ def build_native_smoke(out: str = NATIVE_SMOKE):
     os.replace(tmp, out)
 
 
-STREAM_CEILING = os.path.join(PKG, "stream_ceiling")
+# Measurement programs beside bench.py (not part of the library): built on
+# demand by `bench.py --ceiling` / `bench.py --native`, into _build/.
+BENCH_BUILD = os.path.join(ROOT, "_build")
 
 
-def build_stream_ceiling(out: str = STREAM_CEILING):
-    """The bare-stream HBM ceiling program run by `bench.py --ceiling`."""
+def build_bench_program(name: str) -> str:
+    """Builds bench_ceiling (bare HBM streams) or bench_native (the C ABI
+    from a C++ loop) from the source beside bench.py; returns the path."""
+    if name not in ("bench_ceiling", "bench_native"):
+        raise ValueError(name)
+    os.makedirs(BENCH_BUILD, exist_ok=True)
+    out = os.path.join(BENCH_BUILD, name)
     tmp = out + ".tmp"
+    src = os.path.join(ROOT, name + ".hip")
     flags = [f for f in COMMON if f not in ("-fPIC", "-shared")]
-    _run([HIPCC, *flags, os.path.join(PKG, "csrc", "stream_ceiling.hip"), "-o", tmp])
+    if name == "bench_native":
+        flags += ["-I", os.path.join(ROOT, "include"), "-L", PKG, "-lrip",
+                  "-Wl,-rpath," + PKG]
+    _run([HIPCC, *flags, src, "-o", tmp])
     os.replace(tmp, out)
-
-
-NATIVE_BENCH = os.path.join(PKG, "rip_bench_native")
-
-
-def build_native_bench(out: str = NATIVE_BENCH):
-    """The C-ABI-only throughput program run by `bench.py --native`."""
-    tmp = out + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-Wall",
-          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-I", os.path.join(ROOT, "include"), os.path.join(PKG, "csrc", "rip_bench_native.hip"),
-          "-L", PKG, "-lrip", "-Wl,-rpath,$ORIGIN", "-o", tmp])
-    os.replace(tmp, out)
+    return out
 
 
 def build_all():
     build_librip()
     build_seedgen()
     build_native_smoke()
-    build_stream_ceiling()
-    build_native_bench()
 
 
 if __name__ == "__main__":

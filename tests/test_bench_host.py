@@ -56,3 +56,15 @@ def test_committed_traffic_is_well_formed():
         assert len(e["kernel_hash"]) == 16
         assert 0.999 < e["traffic_over_alg"] < 1.01
         assert e["traffic_bytes_per_launch"] > 0 and e["alg_bytes_per_launch"] > 0
+
+
+def test_cpu_baseline_runs_on_one_core():
+    """The oracle leg pins its thread to one CPU for the timed work and puts
+    the affinity back afterwards."""
+    from seedgen import workloads as wl
+    w = wl.scaled(wl.WORKLOADS[2], [4099])
+    before = os.sched_getaffinity(0)
+    out = bench.cpu_baseline(w, seconds=0.05)
+    assert os.sched_getaffinity(0) == before
+    assert out["cores"] == 1 and out["kind"] == "oracle" and out["value"] > 0
+    assert "pinned to CPU" in out["sample"]

@@ -10,10 +10,12 @@ from collections import deque
 import numpy as np
 import pytest
 
+import test_oracle_draws as td
 import test_oracle_preduce as tp
 import test_oracle_sched as ts
 from oracle import preduce as op
 from oracle import sched as osd
+from oracle import splitmix as osm
 
 PRE_PINS = [
     *[(tp.test_preduce_matches_dense_FG, (s,)) for s in range(6)],
@@ -43,6 +45,25 @@ SCHED_PINS = [
       for a in [(osd.RANDOM_GB, 0), (osd.GD, 0), (osd.GD, 3)]],
     (ts.test_random_group_contains_requester, ()),
     (ts.test_slowdown_filter_rule, ()),
+]
+
+
+def static_row_pin(n, k):
+    with pytest.MonkeyPatch.context() as mp:
+        td.test_static_row_is_a_uniform_partition(n, k, mp)
+
+
+DRAW_PINS = [
+    (td.test_bounded_power_of_two_is_the_top_bits, ()),
+    *[(td.test_bounded_depends_on_the_high_word_only, (n,)) for n in (3, 7, 100)],
+    *[(td.test_shuffle_gives_every_permutation_once, (n,)) for n in (3, 4, 5)],
+    *[(td.test_partial_shuffle_gives_every_ordered_selection_once, a)
+      for a in [(4, 2), (5, 3), (5, 5)]],
+    *[(td.test_random_group_draws_every_subset, a) for a in [(4, 0), (5, 2)]],
+    *[(td.test_global_division_order_is_every_permutation, (n,)) for n in (3, 4)],
+    (td.test_global_division_pairs_are_uniform, ()),
+    *[(td.test_chunks_order_is_every_permutation, (n,)) for n in (3, 4)],
+    *[(static_row_pin, a) for a in [(4, 2), (6, 3)]],
 ]
 
 
@@ -233,3 +254,58 @@ def test_scheduler_mistake_is_caught(label, obj, name, fn):
     assert failures(SCHED_PINS) == 0
     with patched(obj, name, fn):
         assert failures(SCHED_PINS) > 0, f"no pin caught: {label}"
+
+
+# --- mistakes in the seeded draws -------------------------------------------
+def bounded_modulo(self, n):
+    return self.next() % n
+
+
+def bounded_low_bits(self, n):
+    return ((self.next() & 0xFFFFFFFF) * n) >> 32
+
+
+def shuffle_sattolo(items, rng):
+    for a in range(len(items) - 1, 0, -1):
+        b = rng.bounded(a)
+        items[a], items[b] = items[b], items[a]
+    return items
+
+
+def shuffle_stops_early(items, rng):
+    for a in range(len(items) - 1, 1, -1):
+        b = rng.bounded(a + 1)
+        items[a], items[b] = items[b], items[a]
+    return items
+
+
+def shuffle_range_too_wide(items, rng):
+    for a in range(len(items) - 1, 0, -1):
+        b = min(rng.bounded(a + 2), a)
+        items[a], items[b] = items[b], items[a]
+    return items
+
+
+def partial_shuffle_without_offset(items, m, rng):
+    for j in range(m):
+        x = rng.bounded(len(items) - j)
+        items[j], items[x] = items[x], items[j]
+    return items
+
+
+DRAWS = [
+    ("bounded takes the output modulo n", osm.Stream, "bounded", bounded_modulo),
+    ("bounded maps the low 32 bits", osm.Stream, "bounded", bounded_low_bits),
+    ("Sattolo's cyclic shuffle instead of Fisher-Yates", osd, "shuffle", shuffle_sattolo),
+    ("Fisher-Yates stops one position early", osd, "shuffle", shuffle_stops_early),
+    ("Fisher-Yates draws from one slot too many", osd, "shuffle", shuffle_range_too_wide),
+    ("partial shuffle forgets the +j offset", osd, "partial_shuffle",
+     partial_shuffle_without_offset),
+]
+
+
+@pytest.mark.parametrize("label,obj,name,fn", DRAWS, ids=[a[0] for a in DRAWS])
+def test_draw_mistake_is_caught(label, obj, name, fn):
+    assert failures(DRAW_PINS) == 0
+    with patched(obj, name, fn):
+        assert failures(DRAW_PINS) > 0, f"no pin caught: {label}"
