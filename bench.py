@@ -100,7 +100,8 @@ def host_cpu() -> str:
 
 def cpu_baseline(w, seconds: float = 12.0):
     """The oracle as it stands (numpy) on one window of every replica, for as
-    many steps of the workload's schedule as fit the budget (at least 2),
+    many steps of the workload's schedule as fit the budget (at least 2; the
+    schedule runs on past the workload's step count if time is left),
     timed on the update + group averaging only.  It runs on one core: the
     calling thread is pinned to one CPU and numpy's thread pools are limited
     to one thread for the duration (numpy's element-wise operations are
@@ -126,7 +127,7 @@ def cpu_baseline(w, seconds: float = 12.0):
     os.sched_setaffinity(0, {cpu})           # this thread only
     try:
         with threadpool_limits(limits=1):
-            while steps < 2 or (spent < seconds and steps < w.steps):
+            while steps < 2 or spent < seconds:
                 active, groups = sch.step(steps, w.eligible(steps))
                 g = grad(w.grad_slot(steps))
                 t0 = time.perf_counter()

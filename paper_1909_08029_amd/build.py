@@ -88,10 +88,21 @@ def build_bench_program(name: str) -> str:
     return out
 
 
+BF16_CHECK = os.path.join(ROOT, "tests", "native", "libbf16check.so")
+
+
+def build_bf16_check(out: str = BF16_CHECK):
+    """Test helper: the bf16 store conversion against its definition."""
+    tmp = out + ".tmp"
+    _run([HIPCC, *COMMON, os.path.join(ROOT, "tests", "native", "bf16_cvt_check.hip"), "-o", tmp])
+    os.replace(tmp, out)
+
+
 def build_all():
     build_librip()
     build_seedgen()
     build_native_smoke()
+    build_bf16_check()
 
 
 if __name__ == "__main__":

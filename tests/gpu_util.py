@@ -46,7 +46,8 @@ def compare(gpu: np.ndarray, ora: np.ndarray, dtype: int, what: str = ""):
     assert gpu.shape == ora.shape, (gpu.shape, ora.shape)
     g, o = to_f32(gpu, dtype).astype(np.float64), to_f32(ora, dtype).astype(np.float64)
     denom = np.maximum(np.abs(o), 2.0 ** -126)
-    rel = np.abs(g - o) / denom
+    with np.errstate(invalid="ignore"):      # inf - inf where both sides are inf
+        rel = np.abs(g - o) / denom
     rel[(g == o)] = 0.0
     max_rel = float(rel.max()) if rel.size else 0.0
     bits_g = gpu.view(np.uint16 if dtype == DTYPE_BF16 else np.uint32)

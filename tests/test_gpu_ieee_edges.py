@@ -1,0 +1,266 @@
+"""IEEE edge cases of the local update and the group mean, HIP path vs oracle.
+
+The group mean is exact up to the pinned fp32 order (Sec. 3.2: the F^G
+average; Step 4 of Fig. 4 scales the sum by 1/|G|), with no flush of
+subnormals and one round-to-nearest-even when bf16 is stored.  The seeded
+normal-like workload inputs never leave the normal range, so these tests
+build their inputs from the edge classes instead -- subnormal parameters,
+gradients whose product with lr is subnormal, signed zeros, infinities,
+sums that overflow, and (bf16) results that land exactly halfway between
+two bf16 values, including the one that rounds up to infinity -- and put
+them in full tiles and ragged tails of units of 1, 2, 3, 8 and 9 members
+(the specialized paths and the chunked one), with members that do and do
+not update, fp32 and bf16 storage, SGD and momentum, fused and unfused.
+Every stored element must equal the oracle's bit for bit.
+
+The bf16 store is gfx950's v_cvt_pk_bf16_f32 (the fused kernel's device
+code holds it, and no other conversion to bf16; see
+tests/test_kernel_code.py).  test_bf16_store_conversion_all_inputs runs that
+instruction on all 2^32 fp32 patterns against the definition of
+round-to-nearest-even, and a sample of them against the oracle's rounding.
+"""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+
+from seedgen import DTYPE_BF16, DTYPE_F32
+
+from gpu_util import compare, log
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+# groups of 1, 2, 3, 8 and 9 members over replicas 0..22, and two workers
+# (23, 24) that update alone
+GROUPS = [(0,), (1, 2), (3, 4, 5), tuple(range(6, 14)), tuple(range(14, 23))]
+N = 25
+LONE = [23, 24]
+# the first member of every group updates; a few others do not
+IDLE = {4, 13, 16, 19}
+ACTIVE = [r for r in range(N) if r not in IDLE]
+P = 9005   # several tiles of every unit shape, and an element-wise tail
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+# --- inputs -------------------------------------------------------------------
+class Bits:
+    """Random bit patterns of one storage format, by IEEE class (int64
+    arrays of the given shape)."""
+
+    def __init__(self, dtype, rng):
+        self.rng = rng
+        self.mbits = 7 if dtype == DTYPE_BF16 else 23
+        self.sign = np.int64(1) << (self.mbits + 8)
+
+    def make(self, sign, exp, man):
+        return (np.int64(sign) * self.sign) | (np.int64(exp) << self.mbits) | np.int64(man)
+
+    def sign_bits(self, shape):
+        return self.rng.integers(0, 2, shape)
+
+    def normal(self, shape, lo=1, hi=254):
+        r = self.rng
+        return self.make(self.sign_bits(shape), r.integers(lo, hi + 1, shape),
+                         r.integers(0, 1 << self.mbits, shape))
+
+    def subnormal(self, shape):
+        return self.make(self.sign_bits(shape), 0, self.rng.integers(1, 1 << self.mbits, shape))
+
+    def zero(self, shape):
+        return self.make(self.sign_bits(shape), 0, 0)
+
+
+def bits_to_f32(b, dtype):
+    b = np.asarray(b, dtype=np.int64).astype(np.uint32)
+    return (b << np.uint32(16)).view(np.float32) if dtype == DTYPE_BF16 else b.view(np.float32)
+
+
+def f32_to_bits(x, dtype):
+    """Bit patterns of values exactly representable in the storage format."""
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.int64)
+    if dtype == DTYPE_BF16:
+        assert not (b & 0xFFFF).any()
+        return b >> 16
+    return b
+
+
+CASES = ("normal", "subnormal", "zeros", "inf", "overflow", "tie", "mixed")
+
+
+def edge_inputs(dtype, momentum, seed):
+    """param, grad, mom (N x P, stored values) holding, for each unit and
+    element, one of CASES chosen at random:
+      normal     any normal w; g and v of moderate size
+      subnormal  subnormal w and v; g subnormal or below 2^-119, so lr*g is
+                 subnormal (or zero)
+      zeros      signed zeros everywhere
+      inf        the unit's first member holds +-inf, the others finite
+      overflow   every member near the largest finite value, one sign: the
+                 sum of two overflows although the mean would not
+      tie        (units of 1, 2 and 8 members, lr = 1) the mean is exactly
+                 half an ulp of storage above a value b: the first member
+                 has w = k*b and g = -k*h, h = that half ulp, the others
+                 signed zeros; for bf16 a round-to-nearest-even tie, and for
+                 b = the largest bf16 the tie that rounds up to infinity
+      mixed      per member any of normal (no overflow), subnormal, zero
+    No case makes two infinities of opposite sign meet, so no NaN arises."""
+    rng = np.random.default_rng(seed)
+    B = Bits(dtype, rng)
+    w = np.zeros((N, P), dtype=np.int64)
+    g = np.zeros((N, P), dtype=np.int64)
+    v = np.zeros((N, P), dtype=np.int64)
+    for unit in GROUPS + [(r,) for r in LONE]:
+        k = len(unit)
+        sh = (k, P)
+        case = np.broadcast_to(rng.integers(0, len(CASES), P), sh)
+        first = np.zeros(sh, dtype=bool)
+        first[0] = True
+        e_sign = np.broadcast_to(rng.integers(0, 2, P), sh)
+        pick = lambda options: np.choose(rng.integers(0, len(options), sh), options)
+        cand_w = [
+            B.normal(sh),
+            B.subnormal(sh),
+            B.zero(sh),
+            np.where(first, B.make(e_sign, 255, 0), B.normal(sh, 100, 150)),
+            B.make(e_sign, 254, rng.integers(0, 1 << B.mbits, sh)),
+            B.zero(sh),
+            pick([B.normal(sh, 1, 200), B.subnormal(sh), B.zero(sh)]),
+        ]
+        cand_g = [
+            B.normal(sh, 90, 140),
+            np.where(rng.integers(0, 2, sh) == 1, B.subnormal(sh), B.normal(sh, 1, 8)),
+            B.zero(sh),
+            B.normal(sh, 90, 130),
+            B.normal(sh, 1, 100),
+            B.zero(sh),
+            pick([B.normal(sh, 1, 200), B.subnormal(sh), B.zero(sh)]),
+        ]
+        cand_v = [
+            B.normal(sh, 90, 140),
+            B.subnormal(sh),
+            B.zero(sh),
+            B.normal(sh, 90, 130),
+            B.zero(sh),
+            B.zero(sh),
+            pick([B.zero(sh), B.subnormal(sh)]),
+        ]
+        uw, ug, uv = (np.choose(case, c) for c in (cand_w, cand_g, cand_v))
+        if k in (1, 2, 8):
+            tie = case[0] == CASES.index("tie")
+            hi = 254 if k == 1 else 240
+            exp = rng.integers(20, hi + 1, P)
+            man = rng.integers(0, 1 << B.mbits, P)
+            if k == 1:     # now and then the largest finite value
+                top = rng.integers(0, 8, P) == 0
+                exp = np.where(top, 254, exp)
+                man = np.where(top, (1 << B.mbits) - 1, man)
+            b = bits_to_f32(B.make(0, exp, man), dtype)
+            h = np.ldexp(np.float32(1.0), (exp - 127 - B.mbits - 1).astype(np.int32))
+            uw[0] = np.where(tie, f32_to_bits(b * np.float32(k), dtype), uw[0])
+            ug[0] = np.where(tie, f32_to_bits(-h * np.float32(k), dtype), ug[0])
+        for j, m in enumerate(unit):
+            w[m], g[m], v[m] = uw[j], ug[j], uv[j]
+    if dtype == DTYPE_BF16:
+        out = [a.astype(np.uint16) for a in (w, g, v)]
+    else:
+        out = [a.astype(np.uint32).view(np.float32) for a in (w, g, v)]
+    if not momentum:
+        out[2] = None
+    return out
+
+
+# --- device side ----------------------------------------------------------------
+def to_device(a, dtype):
+    import torch
+    if dtype == DTYPE_BF16:
+        t = torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(a.copy())
+    return [[t[r].cuda().contiguous()] for r in range(a.shape[0])]
+
+
+def from_device(rows, dtype):
+    import torch
+    out = []
+    for (t,) in rows:
+        c = t.cpu()
+        out.append(c.view(torch.int16).numpy().view(np.uint16) if dtype == DTYPE_BF16
+                   else c.numpy())
+    return np.stack(out)
+
+
+@pytest.mark.parametrize("lr", [1.0, 0.01])
+@pytest.mark.parametrize("momentum", [0.0, 0.9])
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+def test_edge_values_match_oracle(dtype, fused, momentum, lr):
+    import torch
+    import paper_1909_08029_amd as rip
+    from oracle import preduce as op
+    seed = 1000 + 8 * dtype + 4 * int(fused) + 2 * int(momentum > 0) + int(lr == 1.0)
+    log(f"case ieee edges dtype={dtype} fused={fused} momentum={momentum} lr={lr} seed={seed}")
+    w, g, v = edge_inputs(dtype, momentum, seed)
+    dw, dg = to_device(w, dtype), to_device(g, dtype)
+    dv = to_device(v, dtype) if momentum else None
+    h = rip.Replicas(dw, dg, dv)
+    if fused:
+        rip.rip_preduce(h, GROUPS, ACTIVE, lr=lr, momentum=momentum)
+    else:
+        rip.rip_local_step(h, ACTIVE, lr, momentum)
+        rip.rip_preduce(h, GROUPS)
+    torch.cuda.synchronize()
+    dt = op.BF16 if dtype == DTYPE_BF16 else op.F32
+    with np.errstate(over="ignore", invalid="ignore"):
+        pw, pv = op.step(w, g, v, GROUPS, ACTIVE, lr, momentum or None, dt, fused)
+    got_w = from_device(dw, dtype)
+    f = (pw.astype(np.uint32) << 16).view(np.float32) if dtype == DTYPE_BF16 else pw
+    assert not np.isnan(f).any(), "the cases are built to produce no NaN"
+    # the edge classes reach the stored results
+    assert np.isinf(f).any() and (f == 0).any() and np.signbit(f[f == 0]).any()
+    assert ((f != 0) & (np.abs(f) < np.float32(2.0 ** -126))).any()
+    for r in range(N):
+        compare(got_w[r], pw[r], dtype, f"ieee param r={r}")
+    if momentum:
+        got_v = from_device(dv, dtype)
+        for r in range(N):
+            compare(got_v[r], pv[r], dtype, f"ieee mom r={r}")
+    h.close()
+
+
+def test_bf16_store_conversion_all_inputs():
+    """v_cvt_pk_bf16_f32 equals round-to-nearest-even (NaN: quieted top half)
+    on all 2^32 fp32 patterns; on a sample, it equals the oracle's rounding."""
+    import torch  # noqa: F401  (loads the HIP runtime the helper binds to)
+    from oracle import preduce as op
+    lib = ctypes.CDLL(os.path.join(HERE, "native", "libbf16check.so"))
+    mism = ctypes.c_ulonglong(0)
+    first = (ctypes.c_uint32 * 16)()
+    log("case bf16 conversion, all 2^32 inputs")
+    rc = lib.bf16_cvt_check_all(ctypes.byref(mism), first)
+    assert rc == 0, f"HIP error {rc}"
+    assert mism.value == 0, [hex(x) for x in first[:min(16, mism.value)]]
+
+    rng = np.random.default_rng(5)
+    lows = np.arange(1 << 16, dtype=np.uint32)
+    highs = np.array([0x0000, 0x0001, 0x0080, 0x3F80, 0x3F81, 0x7F7F, 0x7F80, 0x7F81, 0x7FC0,
+                      0x8000, 0x8001, 0xBF80, 0xFF7F, 0xFF80, 0xFFC1], dtype=np.uint32)
+    sample = np.concatenate([(highs[:, None] << 16 | lows[None, :]).ravel(),
+                             rng.integers(0, 1 << 32, 1 << 20, dtype=np.uint32)])
+    out = np.empty(sample.size, dtype=np.uint16)
+    rc = lib.bf16_cvt_apply(sample.ctypes.data_as(ctypes.c_void_p),
+                            out.ctypes.data_as(ctypes.c_void_p), ctypes.c_uint64(sample.size))
+    assert rc == 0, f"HIP error {rc}"
+    want = op.f32_to_bf16(sample.view(np.float32))
+    bad = np.nonzero(out != want)[0]
+    assert bad.size == 0, [(hex(sample[i]), hex(out[i]), hex(want[i])) for i in bad[:8]]
