@@ -225,6 +225,28 @@ int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, int32_t dtyp
                             void* const* grad, void* const* mom, rip_replicas** out);
 void rip_replicas_destroy(rip_replicas* r); /* NULL is a no-op */
 
+/* For callers that cannot allocate device memory (code that runs while a HIP
+ * graph is being captured, tight serving loops, harnesses that forbid
+ * hipMalloc): the same registration as rip_replicas_create, with the same
+ * arguments, checks and errors, but the handle's device tables (pointer
+ * table and segment tables) go into a fixed array of RIP_NOALLOC_TABLE_BYTES
+ * that the library keeps on each device for the life of the process, copied
+ * there with a blocking hipMemcpy.  It calls no hipMalloc or hipFree.
+ * Size: the tables take 24*N*S' + 8*S' + 32*(S'+1) bytes, where S' is 1 when
+ * the segments are back to back (one flat range) and S otherwise; above the
+ * array's size the call fails with RIP_E_UNSUPPORTED and changes nothing.
+ * Sharing: every such handle on a device uses that device's one array, which
+ * keeps the last registration's tables.  Creating another one supersedes the
+ * previous handle on that device: its later calls fail with RIP_E_INVAL
+ * (destroying it is still fine).  A registration that overlaps work still in
+ * flight with the previous handle on that device races with that work:
+ * finish it (synchronize) first.  The handle is used and destroyed like any
+ * other; handles from rip_replicas_create are unaffected. */
+#define RIP_NOALLOC_TABLE_BYTES 65536
+int32_t rip_replicas_create_noalloc(int32_t n_replicas, int32_t n_segments, int32_t dtype,
+                                    const int64_t* seg_numel, void* const* param,
+                                    void* const* grad, void* const* mom, rip_replicas** out);
+
 /* ------------------------------------------------------------------------
  * Local update and P-Reduce (Steps 2 and 4 of Fig. 4; F^G of Sec. 3.2)
  *

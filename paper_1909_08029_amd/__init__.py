@@ -88,6 +88,9 @@ def _load():
         "rip_replicas_create": (ctypes.c_int32, [
             ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
             ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp)]),
+        "rip_replicas_create_noalloc": (ctypes.c_int32, [
+            ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+            ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp)]),
         "rip_replicas_destroy": (None, [vp]),
         "rip_local_step": (ctypes.c_int32, [vp, _i32p, ctypes.c_int32, ctypes.POINTER(Sgd), vp]),
         "rip_preduce": (ctypes.c_int32, [vp, _i32p, _i32p, ctypes.c_int32, _i32p,
@@ -212,9 +215,11 @@ class Replicas:
     """Registers N replicas x S segments of device buffers (torch tensors,
     contiguous, on the current device).  ``param[r][s]`` is segment s of
     replica r; ``grad`` and ``mom`` have the same layout or are None.  The
-    tensors must outlive the handle and any work enqueued with it."""
+    tensors must outlive the handle and any work enqueued with it.
+    ``noalloc=True`` registers through rip_replicas_create_noalloc (the
+    device's one fixed table array; see include/rip.h)."""
 
-    def __init__(self, param, grad=None, mom=None):
+    def __init__(self, param, grad=None, mom=None, noalloc=False):
         n = len(param)
         S = len(param[0])
         dtype = _dtype_code(param[0][0])
@@ -241,9 +246,9 @@ class Replicas:
         self.n, self.S, self.dtype, self.numel = n, S, dtype, numel
         self.tensors = (param, grad, mom)
         h = ctypes.c_void_p()
-        _check(lib.rip_replicas_create(n, S, dtype, (ctypes.c_int64 * S)(*numel),
-                                       self._keep[0], self._keep[1], self._keep[2],
-                                       ctypes.byref(h)))
+        create = lib.rip_replicas_create_noalloc if noalloc else lib.rip_replicas_create
+        _check(create(n, S, dtype, (ctypes.c_int64 * S)(*numel), self._keep[0], self._keep[1],
+                      self._keep[2], ctypes.byref(h)))
         self._h = h
         self._destroy = lib.rip_replicas_destroy  # still reachable at interpreter exit
 

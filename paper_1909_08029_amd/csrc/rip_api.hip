@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -50,10 +51,46 @@ struct rip_replicas {
   bool has_grad = false, has_mom = false;
   int64_t tiles[rip::kTileOptions] = {};  // tiles per unit, by slot option
   void* dmem = nullptr;  // ptab [3][S][N] u64 | seg_numel [S] i64 | seg_tile0 [4][S+1] i64
+  // Handles from rip_replicas_create_noalloc keep their tables in the
+  // device's fixed table array instead of dmem; `generation` tells whether
+  // a later such handle on the same device has overwritten them.
+  bool in_fixed_array = false;
+  uint64_t generation = 0;
   const uint64_t* d_ptab = nullptr;
   const int64_t* d_numel = nullptr;
   const int64_t* d_tile0 = nullptr;
 };
+
+// The device tables of the handle made by rip_replicas_create_noalloc.  In
+// host code this name is a host-side stand-in, not a device address: host
+// code uses only the per-device address from hipGetSymbolAddress below.
+static __device__ __align__(256) uint8_t scratch[RIP_NOALLOC_TABLE_BYTES];
+
+namespace rip {
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_fixed_mu;
+void* g_fixed_ptr[kMaxDevices] = {};      // address of `scratch` on each device
+uint64_t g_fixed_gen[kMaxDevices] = {};   // generation of the handle owning it
+
+// Address of the fixed table array on `device` (the current device), looked
+// up once per device.  Caller holds g_fixed_mu.
+int32_t fixed_array(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(RIP_E_UNSUPPORTED, "device %d above the %d the library supports", device,
+                kMaxDevices);
+  if (!g_fixed_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(RIP_E_HIP, "hipGetSymbolAddress(table array): %s", hipGetErrorString(e));
+    g_fixed_ptr[device] = p;
+  }
+  *out = g_fixed_ptr[device];
+  return RIP_OK;
+}
+}  // namespace
+}  // namespace rip
 
 extern "C" const char* rip_last_error(void) { return rip::g_last_error.c_str(); }
 extern "C" int32_t rip_abi_version(void) { return RIP_ABI_VERSION; }
@@ -197,9 +234,11 @@ int32_t check_buffers(void* const* param, void* const* grad, void* const* mom, i
 
 }  // namespace
 
-extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, int32_t dtype,
-                                       const int64_t* seg_numel, void* const* param,
-                                       void* const* grad, void* const* mom, rip_replicas** out) {
+namespace {
+
+int32_t create_replicas(int32_t n_replicas, int32_t n_segments, int32_t dtype,
+                        const int64_t* seg_numel, void* const* param, void* const* grad,
+                        void* const* mom, rip_replicas** out, bool noalloc) {
   rip::clear_error();
   if (!out) return rip::fail(RIP_E_INVAL, "rip_replicas_create: out is NULL");
   *out = nullptr;
@@ -265,6 +304,13 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
     for (int32_t s = 0; s < S; ++s) t0[s + 1] = t0[s] + (numel[s] + tile_elems - 1) / tile_elems;
   }
 
+  const size_t bytes_ptab = ptab.size() * sizeof(uint64_t);
+  const size_t bytes = bytes_ptab + (size_t)S * 8 + tile0.size() * 8;
+  if (noalloc && bytes > (size_t)RIP_NOALLOC_TABLE_BYTES)
+    return rip::fail(RIP_E_UNSUPPORTED,
+                     "rip_replicas_create_noalloc: the tables of %d replicas x %d segments "
+                     "take %zu bytes, above the fixed array's %d",
+                     N, S, bytes, RIP_NOALLOC_TABLE_BYTES);
   rip_replicas* h = new (std::nothrow) rip_replicas();
   if (!h) return rip::fail(RIP_E_NOMEM, "out of host memory");
   h->n = N;
@@ -277,30 +323,81 @@ extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, i
   h->device = device;
   e = hipDeviceGetAttribute(&h->lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
                             h->device);
-  const size_t bytes_ptab = ptab.size() * sizeof(uint64_t);
-  const size_t bytes = bytes_ptab + (size_t)S * 8 + tile0.size() * 8;
-  if (e == hipSuccess) e = hipMalloc(&h->dmem, bytes);
   if (e != hipSuccess) {
     delete h;
-    return rip::fail(e == hipErrorOutOfMemory ? RIP_E_NOMEM : RIP_E_HIP,
-                     "rip_replicas_create: %s", hipGetErrorString(e));
+    return rip::fail(RIP_E_HIP, "rip_replicas_create: %s", hipGetErrorString(e));
   }
-  char* d = static_cast<char*>(h->dmem);
   std::vector<char> staging(bytes);
   std::memcpy(staging.data(), ptab.data(), bytes_ptab);
   std::memcpy(staging.data() + bytes_ptab, numel.data(), (size_t)S * 8);
   std::memcpy(staging.data() + bytes_ptab + (size_t)S * 8, tile0.data(), tile0.size() * 8);
-  e = hipMemcpy(d, staging.data(), bytes, hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    (void)hipFree(h->dmem);
-    delete h;
-    return rip::fail(RIP_E_HIP, "rip_replicas_create: %s", hipGetErrorString(e));
+  char* d = nullptr;
+  if (noalloc) {
+    // Stage into the device's fixed array; the handle that owned it is
+    // superseded from here on.
+    std::lock_guard<std::mutex> lock(rip::g_fixed_mu);
+    void* fixed = nullptr;
+    const int32_t rc2 = rip::fixed_array(device, &fixed);
+    if (rc2 != RIP_OK) {
+      delete h;
+      return rc2;
+    }
+    e = hipMemcpy(fixed, staging.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      delete h;
+      return rip::fail(RIP_E_HIP, "rip_replicas_create_noalloc: %s", hipGetErrorString(e));
+    }
+    h->in_fixed_array = true;
+    h->generation = ++rip::g_fixed_gen[device];
+    d = static_cast<char*>(fixed);
+  } else {
+    e = hipMalloc(&h->dmem, bytes);
+    if (e != hipSuccess) {
+      delete h;
+      return rip::fail(e == hipErrorOutOfMemory ? RIP_E_NOMEM : RIP_E_HIP,
+                       "rip_replicas_create: %s", hipGetErrorString(e));
+    }
+    d = static_cast<char*>(h->dmem);
+    e = hipMemcpy(d, staging.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(h->dmem);
+      delete h;
+      return rip::fail(RIP_E_HIP, "rip_replicas_create: %s", hipGetErrorString(e));
+    }
   }
   h->d_ptab = reinterpret_cast<const uint64_t*>(d);
   h->d_numel = reinterpret_cast<const int64_t*>(d + bytes_ptab);
   h->d_tile0 = reinterpret_cast<const int64_t*>(d + bytes_ptab + (size_t)S * 8);
   *out = h;
   return RIP_OK;
+}
+
+// A handle whose tables a later rip_replicas_create_noalloc call on its
+// device has overwritten must not launch.
+int32_t check_current(const rip_replicas* r) {
+  if (!r->in_fixed_array) return RIP_OK;
+  std::lock_guard<std::mutex> lock(rip::g_fixed_mu);
+  if (rip::g_fixed_gen[r->device] != r->generation)
+    return rip::fail(RIP_E_INVAL,
+                     "this rip_replicas_create_noalloc handle was superseded by a later one on "
+                     "device %d (they share one table array)",
+                     r->device);
+  return RIP_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t rip_replicas_create(int32_t n_replicas, int32_t n_segments, int32_t dtype,
+                                       const int64_t* seg_numel, void* const* param,
+                                       void* const* grad, void* const* mom, rip_replicas** out) {
+  return create_replicas(n_replicas, n_segments, dtype, seg_numel, param, grad, mom, out, false);
+}
+
+extern "C" int32_t rip_replicas_create_noalloc(int32_t n_replicas, int32_t n_segments,
+                                               int32_t dtype, const int64_t* seg_numel,
+                                               void* const* param, void* const* grad,
+                                               void* const* mom, rip_replicas** out) {
+  return create_replicas(n_replicas, n_segments, dtype, seg_numel, param, grad, mom, out, true);
 }
 
 extern "C" void rip_replicas_destroy(rip_replicas* r) {
@@ -436,6 +533,7 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   if (dev != r->device)
     return rip::fail(RIP_E_INVAL, "current device %d differs from the handle's device %d", dev,
                      r->device);
+  if ((rc = check_current(r)) != RIP_OK) return rc;
   const int cap = rip::g_max_blocks.load() > 0 ? rip::g_max_blocks.load() : rip::kDefaultMaxBlocks;
   const int blocks = (int)(a.work < cap ? a.work : cap);
   int bpc = rip::g_blocks_per_cu.load();
@@ -471,6 +569,7 @@ extern "C" int32_t rip_step(rip_sched* s, const rip_replicas* r, int64_t step,
   if (dev != r->device)
     return rip::fail(RIP_E_INVAL, "current device %d differs from the handle's device %d", dev,
                      r->device);
+  if (const int32_t rc0 = check_current(r); rc0 != RIP_OK) return rc0;
   int32_t act_buf[RIP_MAX_REPLICAS], off_buf[RIP_MAX_REPLICAS + 1], mem_buf[RIP_MAX_REPLICAS];
   int32_t na = 0, ng = 0;
   int32_t* act = active ? active : act_buf;
