@@ -16,7 +16,8 @@
  * Conventions for every call below
  *  - Return value: RIP_OK (0) or a negative RIP_E_* code.  On error nothing
  *    is launched and no caller memory is written, except that the message
- *    returned by rip_last_error() is replaced.  No C++ exception crosses the
+ *    returned by rip_last_error() is replaced (and except a HIP failure of
+ *    the second launch of a split step; see rip_preduce).  No C++ exception crosses the
  *    boundary.
  *  - Host arrays passed in are read during the call only; the caller may
  *    reuse them as soon as the call returns.
@@ -26,10 +27,11 @@
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Device
  *    work is asynchronous on that stream.
  *  - Handles are not thread-safe; use one handle per thread or lock.
- *  - Graph capture: rip_local_step and rip_preduce enqueue exactly one
- *    kernel launch (or nothing, when the step has no work), with the whole
- *    step -- schedule, optimizer scalars, the handle's pointer table -- in
- *    the kernel argument, and no memset, copy or allocation.  They may be
+ *  - Graph capture: rip_local_step and rip_preduce enqueue one kernel
+ *    launch (two for a step that mixes unit shapes with far-apart residency
+ *    preferences; nothing when the step has no work), each with its part of
+ *    the step -- schedule, optimizer scalars, the handle's pointer table --
+ *    in the kernel argument, and no memset, copy or allocation.  They may be
  *    called on a stream under HIP graph capture; each replay re-applies the
  *    captured step to whatever the buffers hold then.  The replicas handle
  *    must outlive the graph.
@@ -286,7 +288,12 @@ int32_t rip_local_step(const rip_replicas* r, const int32_t* active, int32_t n_a
  * of the `n_groups` groups given as CSR (group g = members[group_offsets[g]
  * .. group_offsets[g+1]-1], strictly ascending).  Groups must be disjoint
  * (RIP_E_OVERLAP otherwise).  sgd == NULL is pure P-Reduce; then n_active
- * must be 0.  One kernel launch covers all groups and updates.
+ * must be 0.  One kernel launch covers all groups and updates, or, when the
+ * step's units prefer residency caps far apart (a Global Division step of
+ * pairs and groups of eight, say) and no cap is forced with
+ * rip_set_blocks_per_cu, two launches in a row on `stream`, each at its own
+ * cap; the units are disjoint, so the result is the same either way.  If the
+ * second of two launches fails, the first has been enqueued (RIP_E_HIP).
  * Errors: RIP_E_INVAL (also: the current device is not the handle's),
  * RIP_E_OVERLAP, RIP_E_UNSUPPORTED (a step of 2^31 or more tiles), RIP_E_HIP
  * (launch failure). */
@@ -306,7 +313,8 @@ int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offsets,
  *  active .. n_groups  optional outputs, as in rip_schedule_groups (NULL =
  *             not wanted); written only on success
  * Atomic: on any error (including a failed launch) the scheduler is left as
- * it was, as if the call had not been made, and nothing is launched.
+ * it was, as if the call had not been made, and nothing is launched (a HIP
+ * failure of the second launch of a split step leaves the first enqueued).
  * Errors: RIP_E_INVAL (null handle or sgd, worker counts differ, missing
  * buffers, Nesterov without momentum, device mismatch, a scheduling error),
  * RIP_E_HIP. */

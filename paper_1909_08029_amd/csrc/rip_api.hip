@@ -410,9 +410,15 @@ namespace {
 
 // Checks one step's schedule and turns it into units (groups first, in the
 // order given, then active workers outside every group, ascending).
+// The units' sizes and updating members (for the launch policy).
+struct UnitShapes {
+  int32_t n = 0;
+  int32_t k[RIP_MAX_REPLICAS], act[RIP_MAX_REPLICAS];
+};
+
 int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const int32_t* members,
                    int32_t n_groups, const int32_t* active, int32_t n_active, const rip_sgd* sgd,
-                   rip::StepArgs& a, bool& mom, int& waves) {
+                   rip::StepArgs& a, bool& mom, UnitShapes& shapes) {
   const int32_t N = r->n;
   if (n_groups < 0 || n_active < 0) return rip::fail(RIP_E_INVAL, "negative count");
   if (n_groups > 0 && (!group_offsets || !members))
@@ -502,15 +508,35 @@ int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const in
   for (int32_t u = 1; u < units && a.uniform_tiles; ++u)
     if (a.unit_work0[u + 1] - a.unit_work0[u] != a.uniform_tiles) a.uniform_tiles = 0;
   a.flat_numel = r->n_seg == 1 ? r->numel0 : 0;
-  int32_t unit_k[RIP_MAX_REPLICAS], unit_act[RIP_MAX_REPLICAS];
+  shapes.n = units;
   for (int32_t u = 0; u < units; ++u) {
     const int32_t b = unit_off[u];
-    unit_k[u] = unit_off[u + 1] - b;
-    unit_act[u] = 0;
-    for (int32_t j = 0; j < unit_k[u]; ++j) unit_act[u] += is_active[a.member[b + j]];
+    shapes.k[u] = unit_off[u + 1] - b;
+    shapes.act[u] = 0;
+    for (int32_t j = 0; j < shapes.k[u]; ++j) shapes.act[u] += is_active[a.member[b + j]];
   }
-  waves = rip::policy::launch_waves(unit_k, unit_act, units, mom);
   return RIP_OK;
+}
+
+// The launch of the units u with part[u] == which, in their order: the
+// same member table, active bits and scalars, with the unit tables rebuilt.
+void subset_step(const rip::StepArgs& a, const uint8_t* part, int which, rip::StepArgs& out) {
+  std::memcpy(&out, &a, sizeof a);
+  int32_t n = 0;
+  uint32_t work = 0;
+  out.unit_work0[0] = 0;
+  for (int32_t u = 0; u < a.n_units; ++u) {
+    if (part[u] != which) continue;
+    out.unit_info[n] = a.unit_info[u];
+    work += a.unit_work0[u + 1] - a.unit_work0[u];
+    out.unit_work0[++n] = work;
+  }
+  out.n_units = n;
+  out.work = work;
+  out.uniform_k = 0;  // the units no longer sit at base = unit * k
+  out.uniform_tiles = n > 0 ? out.unit_work0[1] : 0;
+  for (int32_t u = 1; u < n && out.uniform_tiles; ++u)
+    if (out.unit_work0[u + 1] - out.unit_work0[u] != out.uniform_tiles) out.uniform_tiles = 0;
 }
 
 }  // namespace
@@ -522,9 +548,9 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
   if (!r) return rip::fail(RIP_E_INVAL, "rip_preduce: replicas handle is NULL");
   rip::StepArgs a;
   bool mom = false;
-  int waves = 0;
+  UnitShapes shapes;
   int32_t rc =
-      build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a, mom, waves);
+      build_step(r, group_offsets, members, n_groups, active, n_active, sgd, a, mom, shapes);
   if (rc != RIP_OK) return rc;
   if (a.work == 0) return RIP_OK;
   int dev = -1;
@@ -534,17 +560,34 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
     return rip::fail(RIP_E_INVAL, "current device %d differs from the handle's device %d", dev,
                      r->device);
   if ((rc = check_current(r)) != RIP_OK) return rc;
-  const int cap = rip::g_max_blocks.load() > 0 ? rip::g_max_blocks.load() : rip::kDefaultMaxBlocks;
-  const int blocks = (int)(a.work < cap ? a.work : cap);
-  int bpc = rip::g_blocks_per_cu.load();
-  if (bpc == 0) bpc = waves * 64 / rip::kBlock;
-  size_t lds = 0;
-  if (bpc > 0 && r->lds_per_cu > 0) lds = (size_t)(r->lds_per_cu / bpc) & ~(size_t)255;
+  const int max_blocks =
+      rip::g_max_blocks.load() > 0 ? rip::g_max_blocks.load() : rip::kDefaultMaxBlocks;
+  const int forced_bpc = rip::g_blocks_per_cu.load();
   const bool ext = a.wd != 0.0f || a.nesterov != 0;
-  e = rip::launch_fused_step(a, r->dtype == RIP_BF16, mom, ext, blocks, lds,
-                             static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return rip::fail(RIP_E_HIP, "kernel launch: %s", hipGetErrorString(e));
-  return RIP_OK;
+  auto launch = [&](const rip::StepArgs& x, int waves) -> int32_t {
+    if (x.work == 0) return RIP_OK;
+    const int blocks = (int)(x.work < (uint32_t)max_blocks ? x.work : (uint32_t)max_blocks);
+    const int bpc = forced_bpc > 0 ? forced_bpc : waves * 64 / rip::kBlock;
+    size_t lds = 0;
+    if (bpc > 0 && r->lds_per_cu > 0) lds = (size_t)(r->lds_per_cu / bpc) & ~(size_t)255;
+    const hipError_t le = rip::launch_fused_step(x, r->dtype == RIP_BF16, mom, ext, blocks, lds,
+                                                 static_cast<hipStream_t>(stream));
+    if (le != hipSuccess) return rip::fail(RIP_E_HIP, "kernel launch: %s", hipGetErrorString(le));
+    return RIP_OK;
+  };
+  // One launch, or two when the units want residency caps far apart (and
+  // no cap is forced).
+  uint8_t part[RIP_MAX_REPLICAS];
+  int w0 = 0, w1 = 0;
+  if (forced_bpc == 0 &&
+      rip::policy::split_units(shapes.k, shapes.act, shapes.n, mom, part, &w0, &w1)) {
+    rip::StepArgs a0, a1;
+    subset_step(a, part, 0, a0);
+    subset_step(a, part, 1, a1);
+    if ((rc = launch(a0, w0)) != RIP_OK) return rc;
+    return launch(a1, w1);
+  }
+  return launch(a, rip::policy::launch_waves(shapes.k, shapes.act, shapes.n, mom));
 }
 
 extern "C" int32_t rip_step(rip_sched* s, const rip_replicas* r, int64_t step,

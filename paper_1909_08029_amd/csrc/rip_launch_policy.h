@@ -62,5 +62,49 @@ inline int launch_waves(const int32_t* k, const int32_t* act, int32_t units, boo
   return 2 * (int)std::ceil(num / den / 2.0 - 1e-6);
 }
 
+// A step whose units prefer caps far apart (Global Division and Inter-Intra
+// steps mix groups of two to eight, and lone updates, in one launch) runs
+// as two launches, each at the cap of its own units: the units preferring
+// at least kSplitCap waves per CU, then the others.  Only when the step has
+// at least kSplitMinUnits units, each part carries at least kSplitMinShare
+// of the step's bytes, and the parts' caps differ by at least kSplitMinGap;
+// otherwise the second launch's ramp and tail cost more than the better
+// caps gain (steps of one or two random groups).
+constexpr int kSplitCap = 8;
+constexpr int kSplitMinUnits = 3;
+constexpr double kSplitMinShare = 0.15;
+constexpr int kSplitMinGap = 4;
+constexpr int kMaxUnits = 256;  // a launch's units are disjoint, so at most the replicas
+
+// Decides the split of a launch's units.  Returns true and fills part[u]
+// (0: the first launch, preferring >= kSplitCap waves; 1: the second) and
+// the two launches' caps, or returns false (one launch at launch_waves).
+inline bool split_units(const int32_t* k, const int32_t* act, int32_t units, bool mom,
+                        uint8_t* part, int* waves0, int* waves1) {
+  if (units < kSplitMinUnits || units > kMaxUnits) return false;
+  int32_t k0[kMaxUnits], a0[kMaxUnits], k1[kMaxUnits], a1[kMaxUnits];
+  int32_t n0 = 0, n1 = 0;
+  double b0 = 0.0, b1 = 0.0;
+  for (int32_t u = 0; u < units; ++u) {
+    const double bytes = act[u] * (mom ? 5.0 : 3.0) + (k[u] - act[u]) * 2.0;
+    if (unit_waves(k[u], act[u], mom) >= kSplitCap - 1e-9) {
+      part[u] = 0;
+      k0[n0] = k[u];
+      a0[n0++] = act[u];
+      b0 += bytes;
+    } else {
+      part[u] = 1;
+      k1[n1] = k[u];
+      a1[n1++] = act[u];
+      b1 += bytes;
+    }
+  }
+  if (n0 == 0 || n1 == 0) return false;
+  if (b0 < kSplitMinShare * (b0 + b1) || b1 < kSplitMinShare * (b0 + b1)) return false;
+  *waves0 = launch_waves(k0, a0, n0, mom);
+  *waves1 = launch_waves(k1, a1, n1, mom);
+  return *waves0 - *waves1 >= kSplitMinGap;
+}
+
 }  // namespace policy
 }  // namespace rip

@@ -73,6 +73,39 @@ int main() {
             ++g_failures;
           }
         }
+  // Splitting a launch in two.
+  {
+    uint8_t part[16];
+    int w0 = 0, w1 = 0;
+    // one shape: never split
+    std::vector<int32_t> k{4, 4, 4, 4}, a{4, 4, 4, 4};
+    CHECK_EQ(split_units(k.data(), a.data(), 4, false, part, &w0, &w1), 0, "one shape");
+    // too few units
+    k = {2, 8};
+    a = {2, 8};
+    CHECK_EQ(split_units(k.data(), a.data(), 2, true, part, &w0, &w1), 0, "two units");
+    // a Global Division step with momentum: pairs and triples (prefer 10)
+    // against groups of 6-8 (prefer 4-6): split, small groups first
+    k = {2, 3, 8, 6, 2, 7};
+    a = {2, 3, 8, 6, 2, 7};
+    CHECK_EQ(split_units(k.data(), a.data(), 6, true, part, &w0, &w1), 1, "GD with momentum");
+    const int want_part[6] = {0, 0, 1, 1, 0, 1};
+    for (int u = 0; u < 6; ++u) CHECK_EQ(part[u], want_part[u], "GD with momentum: part");
+    {
+      std::vector<int32_t> k0{2, 3, 2}, k1{8, 6, 7};
+      CHECK_EQ(w0, waves(k0, k0, true), "GD with momentum: first cap");
+      CHECK_EQ(w1, waves(k1, k1, true), "GD with momentum: second cap");
+      CHECK_EQ(w0 - w1 >= kSplitMinGap, 1, "GD with momentum: caps far apart");
+    }
+    // one small part below the byte share: no split (a pair beside five groups of eight)
+    k = {2, 8, 8, 8, 8, 8};
+    a = {2, 8, 8, 8, 8, 8};
+    CHECK_EQ(split_units(k.data(), a.data(), 6, true, part, &w0, &w1), 0, "small share");
+    // caps too close: SGD groups of 5 (pref 8) with groups of 7 (8) never split
+    k = {5, 7, 5, 7};
+    a = {5, 7, 5, 7};
+    CHECK_EQ(split_units(k.data(), a.data(), 4, false, part, &w0, &w1), 0, "caps equal");
+  }
   // No units: the default.
   CHECK_EQ(waves({}, {}, false), kWavesDefault, "no units");
   if (g_failures) {

@@ -1,7 +1,7 @@
 """Fused steps captured into a HIP graph replay exactly like eager launches.
 
-Each rip_preduce call enqueues one kernel launch whose argument carries the
-whole step (schedule, optimizer scalars, the handle's pointer-table address)
+Each rip_preduce call enqueues one kernel launch (two for steps that mix far
+apart unit shapes) whose argument carries the whole step (schedule, optimizer scalars, the handle's pointer-table address)
 and does no memset, copy or allocation, so a sequence of steps can be
 captured once and replayed.  The graph is replayed several times with the
 program's own eager work and synchronizations in between; after every replay
