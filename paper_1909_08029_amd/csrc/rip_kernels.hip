@@ -72,20 +72,34 @@ __device__ __forceinline__ void bst16(Rsrc r, int off, u32x4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kNonTemporal);
 }
 
-// The launch tables (the kernel argument's arrays, the registered pointer and
-// segment tables) are never written while a launch runs.  Reading them
-// through the constant address space lets the compiler fetch these
-// wave-uniform values with scalar loads; read as ordinary global memory they
-// become vector loads that wait behind the streaming traffic (the kernel's
-// own stores could alias them, as far as the compiler can tell).
+// The launch tables -- the kernel argument's own arrays (unit tables, member
+// ids, active bits) and the registered pointer and segment tables -- are
+// never written while a launch runs.  Reading them through the constant
+// address space lets the compiler fetch these wave-uniform values with
+// scalar loads, also inside divergent code; read as ordinary global memory
+// they become vector loads that wait behind the streaming traffic (the
+// kernel's own stores could alias them, as far as the compiler can tell).
+// The argument's arrays are read where the argument lives, in the kernel-
+// argument segment (the only explicit argument, at its start), never through
+// the address of a by-value copy, which is private memory in an unoptimized
+// build.
 #define RIP_CONST __attribute__((address_space(4)))
+
+typedef const RIP_CONST StepArgs KArgs;
+__device__ __forceinline__ KArgs& kargs() {
+  return *(KArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+}
 
 template <typename T>
 __device__ __forceinline__ T cld(const T* p, int64_t i) {
   return ((const RIP_CONST T*)p)[i];
 }
-// Byte i of a 4-byte-aligned table, read as its containing dword.
-__device__ __forceinline__ int cld8(const uint8_t* p, int i) {
+template <typename T>
+__device__ __forceinline__ T cld(const RIP_CONST T* p, int64_t i) {
+  return p[i];
+}
+// Byte i of the member table, read as its containing dword.
+__device__ __forceinline__ int cld8(const RIP_CONST uint8_t* p, int i) {
   const uint32_t word = ((const RIP_CONST uint32_t*)p)[i >> 2];
   return (int)((word >> ((i & 3) * 8)) & 0xFFu);
 }
@@ -93,7 +107,7 @@ __device__ __forceinline__ int cld8(const uint8_t* p, int i) {
 // value, byte j in bits 8j..8j+7: one 16-byte scalar load of the aligned
 // dwords that hold them, then a funnel shift.
 typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint64_t cld8x8(const uint8_t* p, int i) {
+__device__ __forceinline__ uint64_t cld8x8(const RIP_CONST uint8_t* p, int i) {
   const u32x4c d = ((const RIP_CONST u32x4c*)p)[i >> 4];
   const u32x4c e = ((const RIP_CONST u32x4c*)p)[(i >> 4) + 1];
   // 32 bytes d|e hold bytes (i & ~15) .. (i & ~15) + 31, which cover i .. i+7
@@ -112,7 +126,7 @@ __device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x 
 // fp32 -> bf16, round to nearest even, NaN kept quiet: gfx950's
 // v_cvt_pk_bf16_f32 (what clang emits for a conversion to __bf16), two values
 // per instruction.  Its results equal the round-to-nearest-even definition
-// for all 2^32 fp32 inputs (checked exhaustively on the GPU).
+// for all 2^32 fp32 inputs (tests/test_gpu_ieee_edges.py runs every one).
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -343,11 +357,11 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
   for (int64_t e = begin + threadIdx.x; e < end; e += kBlock) {
     float s = 0.0f;
     for (int j = 0; j < k; ++j) {
-      const int id = cld8(a.member, base + j);
+      const int id = cld8(kargs().member, base + j);
       const int idx = seg * a.n_rep + id;
       char* w = reinterpret_cast<char*>(cld(a.ptab, idx));
       float x = ld1<BF16>(w, e);
-      if ((cld(a.active_bits, id >> 5) >> (id & 31)) & 1u) {
+      if ((cld(kargs().active_bits, id >> 5) >> (id & 31)) & 1u) {
         const float g = ld1<BF16>(reinterpret_cast<const char*>(cld(a.ptab, plane + idx)), e);
         if constexpr (MOM) {
           char* vp = reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx));
@@ -363,7 +377,7 @@ __device__ void elementwise(const StepArgs& a, int base, int k, int seg, int64_t
     }
     if (k > 1) s = s * inv_k;
     for (int j = 0; j < k; ++j) {
-      const int id = cld8(a.member, base + j);
+      const int id = cld8(kargs().member, base + j);
       st1<BF16>(reinterpret_cast<char*>(cld(a.ptab, seg * a.n_rep + id)), e, s);
     }
   }
@@ -388,7 +402,7 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
   const int off = (int)threadIdx.x * 16;
   float s[N];
   for (int j0 = 0; j0 < k; j0 += C) {
-    const uint64_t ids = cld8x8(a.member, base + j0);  // bytes past the unit are unused
+    const uint64_t ids = cld8x8(kargs().member, base + j0);  // bytes past the unit are unused
     char* w[C];
     const char* g[C];
     char* v[C];
@@ -401,7 +415,7 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
       w[jj] = in ? reinterpret_cast<char*>(cld(a.ptab, idx)) : nullptr;
       g[jj] = in ? reinterpret_cast<const char*>(cld(a.ptab, plane + idx)) : nullptr;
       v[jj] = in && MOM ? reinterpret_cast<char*>(cld(a.ptab, 2 * plane + idx)) : nullptr;
-      act[jj] = in && ((cld(a.active_bits, id >> 5) >> (id & 31)) & 1u);
+      act[jj] = in && ((cld(kargs().active_bits, id >> 5) >> (id & 31)) & 1u);
     }
 #pragma unroll
     for (int jj = 0; jj < C; ++jj) {
@@ -455,7 +469,7 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
   for (int i = 0; i < N; ++i) s[i] = s[i] * inv_k;
   const u32x4 out = V::pack(s);
   for (int j0 = 0; j0 < k; j0 += C) {
-    const uint64_t ids = cld8x8(a.member, base + j0);
+    const uint64_t ids = cld8x8(kargs().member, base + j0);
     char* w[C];
 #pragma unroll
     for (int jj = 0; jj < C; ++jj) {
@@ -471,8 +485,8 @@ __device__ __forceinline__ void wide_tile(const StepArgs& a, int base, int k, in
 }
 
 // Last index i in [0, n) with v[i] <= x (v ascending, v[0] <= x).
-template <typename T, typename X>
-__device__ __forceinline__ int last_le(const T* v, int n, X x) {
+template <typename P, typename X>
+__device__ __forceinline__ int last_le(P v, int n, X x) {
   int lo = 0, hi = n - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -553,13 +567,13 @@ __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
       unit = (int)(w / h.uniform_tiles);
       tile = (int64_t)(w - (uint32_t)unit * h.uniform_tiles);
     } else {
-      unit = last_le(a.unit_work0, a.n_units, w);
-      tile = (int64_t)(w - cld(a.unit_work0, unit));
+      unit = last_le(kargs().unit_work0, a.n_units, w);
+      tile = (int64_t)(w - cld(kargs().unit_work0, unit));
     }
     // With equal-sized units the member window's address needs no load, so
     // it is fetched together with the unit's info word: the unit costs one
     // scalar round trip, its members' pointers a second.
-    const uint32_t info = cld(a.unit_info, unit);
+    const uint32_t info = cld(kargs().unit_info, unit);
     Unit u;
     if (h.uniform_k) {
       u.k = (int)h.uniform_k;
@@ -569,7 +583,7 @@ __global__ __launch_bounds__(kBlock) void fused_step_kernel(StepArgs a) {
       u.base = (int)unit_info_base(info);
     }
     u.act8 = unit_info_act8(info);
-    u.ids = cld8x8(a.member, u.base);
+    u.ids = cld8x8(kargs().member, u.base);
     switch (u.k) {
       case 1: unit_tile<1, BF16, MOM, EXT>(a, h, u, tile); break;
       case 2: unit_tile<2, BF16, MOM, EXT>(a, h, u, tile); break;
