@@ -17,7 +17,8 @@ timed launches: one pair of HIP events on the launch stream brackets the
 whole timed window, and the span is spread evenly over the launches in it
 (the next launch is queued before the previous kernel ends, so the span is
 kernel time plus the dispatch gaps between launches; it can never exceed the
-wall time).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
+wall time; a step that the library runs as two kernels counts as one launch
+there, its bytes and time both whole).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
 same workload, pinned to one core.  Progress goes to stderr.
 """
 from __future__ import annotations
@@ -530,7 +531,8 @@ def main():
             "mean_kernel_us": round(mean_kernel_ms * 1e3, 2),
             "launches_timed": launches,
             "kernel_time": "GPU span of the timed window (one HIP event pair on the launch "
-                           "stream) / launches in it",
+                           "stream) / steps with work in it (a step the library splits into two "
+                           "kernels counts once)",
         },
         "cpu_baseline": cpu,
     }

@@ -1,5 +1,6 @@
 // Practical HBM stream ceilings on this GPU, for the roofline of the fused
-// step kernel.  Each kernel is a bare stream with the fused step's access
+// step kernel (a measurement program beside bench.py: `bench.py --ceiling`
+// builds and runs it; not part of the library).  Each kernel is a bare stream with the fused step's access
 // shape and launch style (single-wave workgroups, one 1 KB-per-stream tile
 // each, non-temporal 16-byte accesses, resident waves per CU capped with a
 // dynamic LDS reservation):

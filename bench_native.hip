@@ -2,9 +2,11 @@
 // no torch.  Registers N flat replicas (parameters, gradients, momentum when
 // asked for) and runs rip_step -- group generation for the step, then the
 // fused local update and P-Reduce in one launch -- for a number of steps,
-// the way a C or C++ training loop would call the library.
+// the way a C or C++ training loop would call the library.  A measurement
+// program beside bench.py (`bench.py --native` builds and runs it), not part
+// of the library.
 //
-//   rip_bench_native [--replicas N] [--params P] [--group K | --fixed a,b,...]
+//   bench_native [--replicas N] [--params P] [--group K | --fixed a,b,...]
 //                    [--momentum M] [--bf16] [--steps S] [--warmup W]
 //
 // --group K: the seeded static schedule (period 4) of groups of K, every
@@ -50,15 +52,15 @@ __global__ void fill_bf16(uint16_t* p, int64_t n, uint64_t seed, float scale) {
 }
 
 int die(const char* what) {
-  std::fprintf(stderr, "rip_bench_native: %s\n", what);
+  std::fprintf(stderr, "bench_native: %s\n", what);
   return 1;
 }
 int die_rip(const char* what, int32_t rc) {
-  std::fprintf(stderr, "rip_bench_native: %s failed (%d): %s\n", what, rc, rip_last_error());
+  std::fprintf(stderr, "bench_native: %s failed (%d): %s\n", what, rc, rip_last_error());
   return 1;
 }
 int die_hip(const char* what, hipError_t e) {
-  std::fprintf(stderr, "rip_bench_native: %s: %s\n", what, hipGetErrorString(e));
+  std::fprintf(stderr, "bench_native: %s: %s\n", what, hipGetErrorString(e));
   return 1;
 }
 
@@ -87,7 +89,7 @@ int main(int argc, char** argv) {
         else if (*p) return die("--fixed takes comma-separated worker ids");
       }
     } else {
-      return die("unknown or incomplete argument (see the header of rip_bench_native.hip)");
+      return die("unknown or incomplete argument (see the header of bench_native.hip)");
     }
   }
   if (n < 1 || n > RIP_MAX_REPLICAS || params < 1 || steps < 1 || warmup < 0)

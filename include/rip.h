@@ -198,7 +198,7 @@ int32_t rip_sched_worker(const rip_sched* s, int32_t worker, rip_worker_state* o
  * Replicas: registered once, used by every step.
  *
  * Each replica r holds S segments (e.g. the layer tensors of a model; the
- * paper flattens them into one buffer per worker, Sec. 5.1 -- here they may
+ * paper flattens them into one buffer per worker, Sec. 6.1 -- here they may
  * stay separate, or be views of one flat buffer).  Segment s has
  * seg_numel[s] elements in every replica.
  *  param  [N*S] host array of device pointers, param[r*S + s]
@@ -266,7 +266,7 @@ int32_t rip_replicas_create_noalloc(int32_t n_replicas, int32_t n_segments, int3
  * once, when stored.  Momentum buffers are never averaged (Step 4 averages
  * parameters only).  momentum == 0 is plain SGD and leaves mom untouched.
  * The paper's ResNet-50 runs use momentum 0.9 and weight decay 1e-4
- * (Sec. 6.1.2); its VGG-16 runs plain SGD.
+ * (Sec. 7.1.2); its VGG-16 runs plain SGD.
  * ---------------------------------------------------------------------- */
 typedef struct rip_sgd {
   float lr;            /* learning rate (eta in Fig. 4) */

@@ -5,7 +5,7 @@ with P-Reduce):
 
   Step 2 (local update), for every worker i that computes this step:
       x_i <- x_i - eta * grad_i
-    With the momentum optimizer the paper uses for ResNet-50 (Sec. 6.1.2,
+    With the momentum optimizer the paper uses for ResNet-50 (Sec. 7.1.2,
     momentum 0.9, weight decay 1e-4), the update is the usual heavy-ball form:
       g <- grad_i + wd * x_i   (when weight decay is on)
       v_i <- mu * v_i + g ;  x_i <- x_i - eta * v_i
@@ -17,7 +17,7 @@ with P-Reduce):
     applied in one step (end of Sec. 3.2).
 
 Precision.  The paper trains in fp32 (its model sizes are quoted as fp32
-bytes, Sec. 6.1.2); replicas are stored as fp32, or as bf16 with fp32
+bytes, Sec. 7.1.2); replicas are stored as fp32, or as bf16 with fp32
 arithmetic.  The oracle therefore computes in fp32, with one fixed order of
 operations so that a correct kernel can match it exactly:
 

@@ -1,6 +1,6 @@
 """Synthetic workloads shaped like the paper's models (recipes only).
 
-The paper trains VGG-16 and ResNet-50 (Sec. 6.1.2); its datasets and weights
+The paper trains VGG-16 and ResNet-50 (Sec. 7.1.2); its datasets and weights
 are not needed to exercise the synchronization path, whose cost depends only
 on the number of replicas, the parameter count, the storage type and the
 schedule.  Each workload below is N replicas of a flat parameter buffer (or
@@ -161,7 +161,7 @@ class DeviceState:
     """All replicas of a workload in device memory.
 
     layout "flat": one buffer per replica and kind, segments are views into
-    it back to back (the zero-copy form of flattening the model, Sec. 5.1).
+    it back to back (the zero-copy form of flattening the model, Sec. 6.1).
     layout "separate": every segment is its own allocation.
     layout "arena": one allocation per kind holding every replica's flat
     buffer at a pitch of (P * element size rounded up to 256 bytes) + pad."""
