@@ -101,6 +101,15 @@ int main() {
     k = {2, 8, 8, 8, 8, 8};
     a = {2, 8, 8, 8, 8, 8};
     CHECK_EQ(split_units(k.data(), a.data(), 6, true, part, &w0, &w1), 0, "small share");
+    // the split step of tests/test_gpu_graph.py: a group of eight beside a
+    // pair and two lone updates, SGD and momentum
+    k = {8, 2, 1, 1};
+    a = {8, 2, 1, 1};
+    for (int mom = 0; mom < 2; ++mom) {
+      CHECK_EQ(split_units(k.data(), a.data(), 4, mom != 0, part, &w0, &w1), 1,
+               "group of eight, pair, two lone updates");
+      CHECK_EQ(part[0], 1, "the group of eight goes second");
+    }
     // caps too close: SGD groups of 5 (pref 8) with groups of 7 (8) never split
     k = {5, 7, 5, 7};
     a = {5, 7, 5, 7};

@@ -18,17 +18,20 @@ from gpu_util import compare, log, oracle_windows
 pytestmark = pytest.mark.gpu
 
 # (active, groups) per captured step: grouped and lone updates, a group whose
-# members do not all update, and a pure P-Reduce of everyone
+# members do not all update, a pure P-Reduce of six, and a step that the
+# library splits into two launches (a group of eight, which wants few
+# resident waves, beside a pair and two lone updates, which want many)
 STEPS = [
     ([0, 1, 2, 3, 4, 5], [(0, 1, 2), (3, 4)]),
     ([0, 2, 3], [(1, 5), (2, 3)]),
     ([], [(0, 1, 2, 3, 4, 5)]),
+    (list(range(12)), [tuple(range(8)), (8, 9)]),
 ]
 
 
 def _workload(dtype, momentum):
     return wl.Workload(f"graph_{'bf16' if dtype else 'fp32'}_{'mom' if momentum else 'sgd'}",
-                       6, [3 * 4096 + 5], dtype, 0.1 if not dtype else 2.0, momentum,
+                       12, [3 * 4096 + 5], dtype, 0.1 if not dtype else 2.0, momentum,
                        0.01, dict(mode=wl.TABLE, table=[[(0, 1)]]), len(STEPS), 7,
                        param_sigma=1.0 if not dtype else 0.05, grad_ring=1)
 
