@@ -17,8 +17,8 @@
  *  - Return value: RIP_OK (0) or a negative RIP_E_* code.  On error nothing
  *    is launched and no caller memory is written, except that the message
  *    returned by rip_last_error() is replaced (and except a HIP failure of
- *    the second launch of a split step; see rip_preduce).  No C++ exception crosses the
- *    boundary.
+ *    the second launch of a split step; see rip_preduce).  No C++ exception
+ *    crosses the boundary.
  *  - Host arrays passed in are read during the call only; the caller may
  *    reuse them as soon as the call returns.
  *  - Device buffers (parameters, gradients, momentum) belong to the caller.
@@ -236,7 +236,9 @@ void rip_replicas_destroy(rip_replicas* r); /* NULL is a no-op */
  * there with a blocking hipMemcpy.  It calls no hipMalloc or hipFree.
  * Size: the tables take 24*N*S' + 8*S' + 32*(S'+1) bytes, where S' is 1 when
  * the segments are back to back (one flat range) and S otherwise; above the
- * array's size the call fails with RIP_E_UNSUPPORTED and changes nothing.
+ * array's size the call fails with RIP_E_UNSUPPORTED and changes nothing
+ * (a failure of the copy itself, RIP_E_HIP, still supersedes the previous
+ * handle).
  * Sharing: every such handle on a device uses that device's one array, which
  * keeps the last registration's tables.  Creating another one supersedes the
  * previous handle on that device: its later calls fail with RIP_E_INVAL

@@ -333,8 +333,9 @@ int32_t create_replicas(int32_t n_replicas, int32_t n_segments, int32_t dtype,
   std::memcpy(staging.data() + bytes_ptab + (size_t)S * 8, tile0.data(), tile0.size() * 8);
   char* d = nullptr;
   if (noalloc) {
-    // Stage into the device's fixed array; the handle that owned it is
-    // superseded from here on.
+    // Stage into the device's fixed array.  The handle that owned it is
+    // superseded before the copy starts, so that a failed copy cannot leave
+    // it pointing at half-written tables.
     std::lock_guard<std::mutex> lock(rip::g_fixed_mu);
     void* fixed = nullptr;
     const int32_t rc2 = rip::fixed_array(device, &fixed);
@@ -342,13 +343,14 @@ int32_t create_replicas(int32_t n_replicas, int32_t n_segments, int32_t dtype,
       delete h;
       return rc2;
     }
+    const uint64_t generation = ++rip::g_fixed_gen[device];
     e = hipMemcpy(fixed, staging.data(), bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       delete h;
       return rip::fail(RIP_E_HIP, "rip_replicas_create_noalloc: %s", hipGetErrorString(e));
     }
     h->in_fixed_array = true;
-    h->generation = ++rip::g_fixed_gen[device];
+    h->generation = generation;
     d = static_cast<char*>(fixed);
   } else {
     e = hipMalloc(&h->dmem, bytes);
@@ -408,14 +410,14 @@ extern "C" void rip_replicas_destroy(rip_replicas* r) {
 
 namespace {
 
-// Checks one step's schedule and turns it into units (groups first, in the
-// order given, then active workers outside every group, ascending).
 // The units' sizes and updating members (for the launch policy).
 struct UnitShapes {
   int32_t n = 0;
   int32_t k[RIP_MAX_REPLICAS], act[RIP_MAX_REPLICAS];
 };
 
+// Checks one step's schedule and turns it into units (groups first, in the
+// order given, then active workers outside every group, ascending).
 int32_t build_step(const rip_replicas* r, const int32_t* group_offsets, const int32_t* members,
                    int32_t n_groups, const int32_t* active, int32_t n_active, const rip_sgd* sgd,
                    rip::StepArgs& a, bool& mom, UnitShapes& shapes) {
