@@ -1,8 +1,8 @@
 """Pins for the oracle's seeded draws (CPU only).
 
 The group generator's random choices -- static rows (Sec. 4.2), random groups
-(Step 3 of Fig. 4), Global Division (Sec. 5.1) and the Inter-Intra division
-(Sec. 5.2) -- come from three pieces:
+(Step 3 of Fig. 4), Global Division (Sec. 5.1), the Inter-Intra division
+(Sec. 5.2) and AD-PSGD's partners (Fig. 3) -- come from three pieces:
 
   bounded(n)        Lemire's multiply-shift map of a SplitMix64 output onto
                     [0, n): it uses the high 32 bits of the output;
@@ -15,8 +15,8 @@ and a shuffle driven through *every* possible draw sequence produces every
 permutation (every ordered selection) exactly once -- the bijection that makes
 Fisher-Yates uniform, which Sattolo's variant, off-by-one ranges and a
 partial shuffle that forgets its offset all break.  The scheduler's uses of
-them (static rows, random groups, divisions, chunks) are enumerated the same
-way end to end.
+them (static rows, random groups, divisions, chunks, Inter-Intra heads,
+AD-PSGD partners) are enumerated the same way end to end.
 """
 import itertools
 import math
@@ -222,3 +222,33 @@ def test_static_row_is_a_uniform_partition(n, k, monkeypatch):
     assert sum(runs.values()) == math.factorial(n)
     assert set(runs) == set(parts)
     assert set(runs.values()) == {math.factorial(n) // len(parts)}
+
+
+@pytest.mark.parametrize("n,i", [(2, 1), (4, 0), (5, 3)])
+def test_adpsgd_partner_is_every_other_worker_once(n, i):
+    """AD-PSGD (Fig. 3): the requester's passive partner is a uniform draw
+    over the other workers -- each exactly once over every draw sequence."""
+    def run(s):
+        sch = with_stream(osd.Scheduler(n, osd.ADPSGD), s)
+        (g,) = sch._adpsgd_step([i])
+        return g
+
+    runs = every_draw_sequence(run)
+    assert sorted(runs) == sorted(tuple(sorted((i, j))) for j in range(n) if j != i)
+
+
+def test_inter_intra_heads_and_their_order():
+    """Inter-Intra (Sec. 5.2), 2 nodes of 2 workers, groups of one: each node's
+    head is either of its idle workers and the two heads come in either
+    order -- each of the 2 x 2 x 2 outcomes from exactly one draw sequence;
+    each node's intra-phase group is the whole node."""
+    def run(s):
+        sch = with_stream(osd.Scheduler(4, osd.INTER_INTRA, kmin=1, kmax=1, n_nodes=2), s)
+        sch._inter_intra_division(0)
+        made = [g for _, g in sorted(sch.groups.items())]
+        assert made[-2:] == [(0, 1), (2, 3)]
+        return made[0][0], made[1][0]
+
+    runs = every_draw_sequence(run)
+    want = [(a, b) for h0 in (0, 1) for h1 in (2, 3) for a, b in ((h0, h1), (h1, h0))]
+    assert sorted(runs) == sorted(want)

@@ -64,6 +64,8 @@ DRAW_PINS = [
     (td.test_global_division_pairs_are_uniform, ()),
     *[(td.test_chunks_order_is_every_permutation, (n,)) for n in (3, 4)],
     *[(static_row_pin, a) for a in [(4, 2), (6, 3)]],
+    *[(td.test_adpsgd_partner_is_every_other_worker_once, a) for a in [(4, 0), (5, 3)]],
+    (td.test_inter_intra_heads_and_their_order, ()),
 ]
 
 
@@ -293,6 +295,54 @@ def partial_shuffle_without_offset(items, m, rng):
     return items
 
 
+ORIG_ADPSGD = osd.Scheduler._adpsgd_step
+ORIG_INTER_INTRA = osd.Scheduler._inter_intra_division
+
+
+def adpsgd_partner_may_be_self(self, active):
+    # draws the partner over all n workers instead of the n-1 others
+    for i in active:
+        self.c[i] += 1
+        if self.n == 1:
+            self.skips[i] += 1
+            continue
+        self.partner[i] = self.rng.bounded(self.n - 1)
+        self.seq[i] = self.next_id
+        self.next_id += 1
+        self.waiting[i] = True
+    locked, executed = set(), []
+    for i in sorted((w for w in range(self.n) if self.waiting[w]), key=lambda w: self.seq[w]):
+        j = self.partner[i]
+        if i in locked or j in locked:
+            continue
+        locked |= {i, j}
+        self.waiting[i] = False
+        self.syncs[i] += 1
+        executed.append(tuple(sorted({i, j})))
+    return executed
+
+
+def inter_intra_first_worker_heads(self, i):
+    # the head of each node is always its first idle worker, not a draw
+    # (the division draws the heads first, one per node)
+    rng = self.rng
+    idle = [w for w in range(self.n) if not self.gb[w]]
+    nodes = len({w // self.per_node for w in idle})
+    calls = {"n": 0}
+
+    class Wrapped:
+        def bounded(self, n):
+            calls["n"] += 1
+            if calls["n"] <= nodes:
+                return 0
+            return rng.bounded(n)
+    self.rng = Wrapped()
+    try:
+        ORIG_INTER_INTRA(self, i)
+    finally:
+        self.rng = rng
+
+
 DRAWS = [
     ("bounded takes the output modulo n", osm.Stream, "bounded", bounded_modulo),
     ("bounded maps the low 32 bits", osm.Stream, "bounded", bounded_low_bits),
@@ -301,6 +351,10 @@ DRAWS = [
     ("Fisher-Yates draws from one slot too many", osd, "shuffle", shuffle_range_too_wide),
     ("partial shuffle forgets the +j offset", osd, "partial_shuffle",
      partial_shuffle_without_offset),
+    ("AD-PSGD partner drawn without skipping the requester", osd.Scheduler, "_adpsgd_step",
+     adpsgd_partner_may_be_self),
+    ("Inter-Intra head is always the node's first idle worker", osd.Scheduler,
+     "_inter_intra_division", inter_intra_first_worker_heads),
 ]
 
 
