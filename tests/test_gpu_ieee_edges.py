@@ -10,8 +10,10 @@ sums that overflow, and (bf16) results that land exactly halfway between
 two bf16 values, including the one that rounds up to infinity -- and put
 them in full tiles and ragged tails of units of 1, 2, 3, 8 and 9 members
 (the specialized paths and the chunked one), with members that do and do
-not update, fp32 and bf16 storage, SGD and momentum, fused and unfused.
-Every stored element must equal the oracle's bit for bit.
+not update, fp32 and bf16 storage, SGD and momentum, fused and unfused; and,
+through the kernel variant with weight decay and Nesterov momentum, NaN
+inputs.  Every stored element must equal the oracle's bit for bit (a NaN
+only in being NaN: its sign and payload after arithmetic are the hardware's).
 
 The bf16 store is gfx950's v_cvt_pk_bf16_f32 (the fused kernel's device
 code holds it, and no other conversion to bf16; see
@@ -235,6 +237,56 @@ def test_edge_values_match_oracle(dtype, fused, momentum, lr):
         got_v = from_device(dv, dtype)
         for r in range(N):
             compare(got_v[r], pv[r], dtype, f"ieee mom r={r}")
+    h.close()
+
+
+def compare_nan_aware(gpu, ora, dtype, what):
+    """NaN where the oracle has NaN (any sign or payload: the hardware's and
+    the host's quieting of an arithmetic NaN differ), bit-exact elsewhere."""
+    from gpu_util import to_f32
+    gf, of = to_f32(gpu, dtype), to_f32(ora, dtype)
+    nan = np.isnan(of)
+    assert np.array_equal(np.isnan(gf), nan), f"{what}: NaN positions differ"
+    compare(gpu[~nan], ora[~nan], dtype, what)
+    return int(nan.sum())
+
+
+@pytest.mark.parametrize("wd,nesterov", [(1e-2, False), (1e-2, True), (0.0, True)])
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+def test_nan_inputs_and_decay_nesterov_edges(dtype, wd, nesterov):
+    """The kernel variant with weight decay and Nesterov momentum on the same
+    edge values, plus NaN parameters and gradients scattered through the
+    units: a NaN input makes its unit's mean NaN and nothing else, and
+    weight decay on an infinite parameter makes inf - inf = NaN, as in the
+    oracle; every other element matches bit for bit."""
+    import torch
+    import paper_1909_08029_amd as rip
+    from oracle import preduce as op
+    seed = 2000 + 8 * dtype + 2 * int(nesterov) + int(wd > 0)
+    log(f"case ieee nan dtype={dtype} wd={wd} nesterov={nesterov} seed={seed}")
+    w, g, v = edge_inputs(dtype, 0.9, seed)
+    rng = np.random.default_rng(seed)
+    qnan = 0x7FC0 if dtype == DTYPE_BF16 else 0x7FC00000
+    mbits = 7 if dtype == DTYPE_BF16 else 23
+    for arr in (w, g):
+        bits = arr.view(np.uint16 if dtype == DTYPE_BF16 else np.uint32)
+        pick = rng.random(bits.shape) < 0.01
+        payload = rng.integers(0, 1 << (mbits - 1), bits.shape).astype(bits.dtype)
+        sign = (rng.integers(0, 2, bits.shape) << (mbits + 8)).astype(bits.dtype)
+        bits[pick] = (qnan | payload | sign)[pick]
+    dw, dg, dv = to_device(w, dtype), to_device(g, dtype), to_device(v, dtype)
+    h = rip.Replicas(dw, dg, dv)
+    rip.rip_preduce(h, GROUPS, ACTIVE, lr=0.5, momentum=0.9, weight_decay=wd, nesterov=nesterov)
+    torch.cuda.synchronize()
+    dt = op.BF16 if dtype == DTYPE_BF16 else op.F32
+    with np.errstate(over="ignore", invalid="ignore"):
+        pw, pv = op.step(w, g, v, GROUPS, ACTIVE, 0.5, 0.9, dt, True, wd, nesterov)
+    got_w, got_v = from_device(dw, dtype), from_device(dv, dtype)
+    nans = 0
+    for r in range(N):
+        nans += compare_nan_aware(got_w[r], pw[r], dtype, f"ieee nan param r={r}")
+        compare_nan_aware(got_v[r], pv[r], dtype, f"ieee nan mom r={r}")
+    assert nans > 0
     h.close()
 
 
