@@ -245,7 +245,10 @@ void rip_replicas_destroy(rip_replicas* r); /* NULL is a no-op */
  * (destroying it is still fine).  A registration that overlaps work still in
  * flight with the previous handle on that device races with that work:
  * finish it (synchronize) first.  The handle is used and destroyed like any
- * other; handles from rip_replicas_create are unaffected. */
+ * other; handles from rip_replicas_create are unaffected.  The registration
+ * itself copies synchronously, so it is made outside a stream capture; the
+ * rip_preduce / rip_local_step / rip_step launches that use the handle may
+ * then be captured like any others. */
 #define RIP_NOALLOC_TABLE_BYTES 65536
 int32_t rip_replicas_create_noalloc(int32_t n_replicas, int32_t n_segments, int32_t dtype,
                                     const int64_t* seg_numel, void* const* param,
