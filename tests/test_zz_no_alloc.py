@@ -5,7 +5,8 @@ Two registrations in a row on one device (the second smaller: fewer
 replicas, fewer elements, another storage type), each checked bit for bit
 against a handle from rip_replicas_create running the same step on a copy of
 the same inputs; the superseded handle is refused without touching memory;
-tables above the fixed array's size are refused.
+tables above the fixed array's size are refused; and steps on such a handle
+captured into a HIP graph replay like eager steps on an allocating handle.
 """
 import numpy as np
 import pytest
@@ -93,3 +94,31 @@ def test_noalloc_rejects_tables_above_its_size():
     assert exc.value.code == rip.RIP_E_UNSUPPORTED
     # the same registration through the allocating entry point works
     rip.Replicas(param, None, None).close()
+
+
+def test_noalloc_handle_launches_replay_from_a_graph():
+    """The use it is for: register once without allocating, capture the
+    steps into a HIP graph, replay; each replay equals eager steps on an
+    allocating handle."""
+    import torch
+    import paper_1909_08029_amd as rip
+    torch.cuda.set_device(0)
+    w, groups, active = CALLS[0]
+    log(f"case noalloc graph: N={w.n} P={w.numel}")
+    a, b = state(w), state(w)
+    ha = rip.Replicas(a.param, a.grad_sets[0], a.mom)
+    hb = rip.Replicas(b.param, b.grad_sets[0], b.mom, noalloc=True)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        rip.rip_preduce(hb, groups, active, lr=w.lr, momentum=w.momentum,
+                        stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for rep in range(3):
+        g.replay()
+        run_step(ha, w, groups, active)
+        torch.cuda.synchronize()
+        check_same(a, b, w, f"graph replay {rep}")
+    del g
+    ha.close()
+    hb.close()
