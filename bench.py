@@ -519,6 +519,7 @@ def main():
             "pass": "unfused (local step, then P-Reduce)" if args.unfused else "fused",
             "launch": (f"hip graph of {graph_period} steps, replayed" if graph_period
                        else "one library call per step"),
+            **({"note": w.note} if w.note else {}),
         },
         "roofline": {
             "bound": "hbm",
