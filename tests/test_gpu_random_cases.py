@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
 
 # RIP_RANDOM_CASES raises the count for a longer one-off run; RIP_RANDOM_SCALE
 # multiplies the segment sizes and RIP_RANDOM_MAX_N raises the replica count.
-CASES = int(os.environ.get("RIP_RANDOM_CASES", "96"))
+CASES = int(os.environ.get("RIP_RANDOM_CASES", "400"))
 SCALE = int(os.environ.get("RIP_RANDOM_SCALE", "1"))
 MAX_N = int(os.environ.get("RIP_RANDOM_MAX_N", "40"))
 
