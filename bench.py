@@ -402,32 +402,43 @@ def main():
 
     stats = dict(steps=0, updates=0, groups=0, members=0, empty=0)
 
-    def one_step(timed=False):
-        """One step; returns (algorithmic bytes, kernel launches)."""
+    opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
+               nesterov=w.nesterov)
+    eligible = [w.eligible(i) for i in range(args.warmup + args.steps)]
+
+    def one_step():
+        """One step; returns its (active, groups).  Bytes and statistics are
+        worked out after the timed window, so the loop holds only the calls."""
         nonlocal t
         h = handles[w.grad_slot(t)]
-        opt = dict(momentum=w.momentum, stream=stream, weight_decay=w.weight_decay,
-                   nesterov=w.nesterov)
         if args.unfused:
-            active, groups = rip.rip_schedule_groups(sched, t, w.eligible(t))
+            active, groups = rip.rip_schedule_groups(sched, t, eligible[t])
             if active:
                 rip.rip_local_step(h, active, w.lr, **opt)
             rip.rip_preduce(h, groups, stream=stream)
-            launches = int(bool(active)) + int(any(len(g) > 1 for g in groups))
         else:
             # group generation and the fused launch in one library call
-            active, groups = rip.rip_step(sched, h, t, w.lr, eligible=w.eligible(t), **opt)
-            launches = int(bool(active) or any(len(g) > 1 for g in groups))
-        if timed:
+            active, groups = rip.rip_step(sched, h, t, w.lr, eligible=eligible[t], **opt)
+        t += 1
+        return active, groups
+
+    def account(done):
+        """Algorithmic bytes and steps with work of the timed steps."""
+        total, launched = 0, 0
+        for active, groups in done:
             stats["steps"] += 1
             stats["updates"] += len(active)
             stats["groups"] += sum(1 for g in groups if len(g) > 1)
             stats["members"] += sum(len(g) for g in groups if len(g) > 1)
-            stats["empty"] += 0 if (active or any(len(g) > 1 for g in groups)) else 1
-        t += 1
-        if args.unfused:
-            return w.alg_bytes_unfused(active, groups), launches
-        return w.alg_bytes(active, groups), launches
+            work = bool(active) or any(len(g) > 1 for g in groups)
+            stats["empty"] += 0 if work else 1
+            if args.unfused:
+                total += w.alg_bytes_unfused(active, groups)
+                launched += int(bool(active)) + int(any(len(g) > 1 for g in groups))
+            else:
+                total += w.alg_bytes(active, groups)
+                launched += int(work)
+        return total, launched
 
     for _ in range(args.warmup):
         one_step()
@@ -445,18 +456,17 @@ def main():
         # stream: markers between steps would add packets to the stream.
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        total_bytes, launches = 0, 0
+        done = [None] * args.steps
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         e0.record(stream)
         for i in range(args.steps):
-            b, n_launch = one_step(timed=True)
-            total_bytes += b
-            launches += n_launch
+            done[i] = one_step()
         e1.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         span_ms = e0.elapsed_time(e1)
+        total_bytes, launches = account(done)
     err(f"[bench] {args.steps} timed steps: {wall * 1e3:.2f} ms wall, "
         f"{span_ms:.2f} ms GPU span, {launches} launches")
 

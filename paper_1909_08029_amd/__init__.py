@@ -9,6 +9,7 @@ fallback.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 from typing import List, Optional, Sequence, Tuple
 
@@ -65,6 +66,13 @@ class WorkerState(ctypes.Structure):
 class Sgd(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float),
                 ("weight_decay", ctypes.c_float), ("nesterov", ctypes.c_int32)]
+
+
+@functools.lru_cache(maxsize=64)
+def _sgd(lr: float, momentum: float, weight_decay: float, nesterov: bool) -> Sgd:
+    """The optimizer struct for these values, built once (the library only
+    reads it), so a loop of steps does not rebuild it every call."""
+    return Sgd(lr, momentum, weight_decay, int(bool(nesterov)))
 
 
 def _load():
@@ -271,7 +279,7 @@ def rip_local_step(rep: Replicas, active: Sequence[int], lr: float, momentum: fl
                    stream=None, weight_decay: float = 0.0, nesterov: bool = False) -> None:
     """Step 2 of Fig. 4 for the listed workers (see include/rip.h)."""
     act = _i32_array(list(active))
-    sgd = Sgd(lr, momentum, weight_decay, int(bool(nesterov)))
+    sgd = _sgd(lr, momentum, weight_decay, bool(nesterov))
     _check(lib.rip_local_step(rep._h, act, len(active), ctypes.byref(sgd),
                               _stream_ptr(stream)))
 
@@ -284,7 +292,7 @@ def rip_preduce(rep: Replicas, groups: Sequence[Sequence[int]], active: Sequence
     off, mem = _csr(groups)
     act = _i32_array(list(active))
     sgd = None if lr is None else ctypes.byref(
-        Sgd(lr, momentum, weight_decay, int(bool(nesterov))))
+        _sgd(lr, momentum, weight_decay, bool(nesterov)))
     _check(lib.rip_preduce(rep._h, off, mem, len(groups), act, len(active), sgd,
                            _stream_ptr(stream)))
 
@@ -297,7 +305,7 @@ def rip_step(sched: Scheduler, rep: Replicas, step: int, lr: float, momentum: fl
     el = None if eligible is None else bytes(1 if e else 0 for e in eligible)
     if el is not None and len(el) != sched.n:
         raise ValueError("eligible must have one entry per worker")
-    sgd = Sgd(lr, momentum, weight_decay, int(bool(nesterov)))
+    sgd = _sgd(lr, momentum, weight_decay, bool(nesterov))
     _check(lib.rip_step(sched._h, rep._h, step, el, ctypes.byref(sgd), _stream_ptr(stream),
                         sched._act, ctypes.byref(sched._na), sched._off, sched._mem,
                         ctypes.byref(sched._ng)))
