@@ -17,8 +17,8 @@ timed launches: one pair of HIP events on the launch stream brackets the
 whole timed window, and the span is spread evenly over the launches in it
 (the next launch is queued before the previous kernel ends, so the span is
 kernel time plus the dispatch gaps between launches; it can never exceed the
-wall time; a step that the library runs as two kernels counts as one launch
-there, its bytes and time both whole).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
+wall time; the library reports how many kernels each step enqueued, one or
+two).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
 same workload, pinned to one core.  Progress goes to stderr.
 """
 from __future__ import annotations
@@ -154,7 +154,8 @@ def graph_steps(args, w, rip, handles, sched, t, stream, stats):
     launches captured into a HIP graph, and a second scheduler checks that the
     next period schedules exactly the same groups.  Every replay then runs
     those steps, as a static schedule prescribes.  Returns (period,
-    bytes per step, GPU span in ms of all replays, wall seconds)."""
+    bytes per step, GPU span in ms of all replays, wall seconds, kernel
+    launches replayed)."""
     import math
     import torch
     from seedgen import workloads as wl
@@ -181,11 +182,13 @@ def graph_steps(args, w, rip, handles, sched, t, stream, stats):
     opt = dict(momentum=w.momentum, weight_decay=w.weight_decay, nesterov=w.nesterov)
     g = torch.cuda.CUDAGraph()
     torch.cuda.synchronize()
+    kernels = 0
     with torch.cuda.graph(g):
         cap = torch.cuda.current_stream()
         for i, (active, groups) in enumerate(period):
             rip.rip_preduce(handles[w.grad_slot(t + i)], groups, active, lr=w.lr, stream=cap,
                             **opt)
+            kernels += rip.rip_last_launch_count()
     torch.cuda.synchronize()
     g.replay()                                     # first execution, untimed
     torch.cuda.synchronize()
@@ -212,7 +215,7 @@ def graph_steps(args, w, rip, handles, sched, t, stream, stats):
             stats["members"] += sum(len(x) for x in groups if len(x) > 1)
             stats["empty"] += 0 if (active or any(len(x) > 1 for x in groups)) else 1
     del g
-    return L, per_step_bytes, span_ms, wall
+    return L, per_step_bytes, span_ms, wall, kernels * reps
 
 
 def sweep_caps(args, w, rip, handles, stream):
@@ -411,33 +414,32 @@ def main():
         worked out after the timed window, so the loop holds only the calls."""
         nonlocal t
         h = handles[w.grad_slot(t)]
+        kernels = 0
         if args.unfused:
             active, groups = rip.rip_schedule_groups(sched, t, eligible[t])
             if active:
                 rip.rip_local_step(h, active, w.lr, **opt)
+                kernels += rip.rip_last_launch_count()
             rip.rip_preduce(h, groups, stream=stream)
         else:
             # group generation and the fused launch in one library call
             active, groups = rip.rip_step(sched, h, t, w.lr, eligible=eligible[t], **opt)
+        kernels += rip.rip_last_launch_count()
         t += 1
-        return active, groups
+        return active, groups, kernels
 
     def account(done):
-        """Algorithmic bytes and steps with work of the timed steps."""
+        """Algorithmic bytes and kernel launches of the timed steps."""
         total, launched = 0, 0
-        for active, groups in done:
+        for active, groups, kernels in done:
             stats["steps"] += 1
             stats["updates"] += len(active)
             stats["groups"] += sum(1 for g in groups if len(g) > 1)
             stats["members"] += sum(len(g) for g in groups if len(g) > 1)
             work = bool(active) or any(len(g) > 1 for g in groups)
             stats["empty"] += 0 if work else 1
-            if args.unfused:
-                total += w.alg_bytes_unfused(active, groups)
-                launched += int(bool(active)) + int(any(len(g) > 1 for g in groups))
-            else:
-                total += w.alg_bytes(active, groups)
-                launched += int(work)
+            total += (w.alg_bytes_unfused if args.unfused else w.alg_bytes)(active, groups)
+            launched += kernels
         return total, launched
 
     for _ in range(args.warmup):
@@ -447,10 +449,9 @@ def main():
 
     graph_period = 0
     if args.graph:
-        graph_period, per_step_bytes, span_ms, wall = graph_steps(
+        graph_period, per_step_bytes, span_ms, wall, launches = graph_steps(
             args, w, rip, handles, sched, t, stream, stats)
         total_bytes = sum(per_step_bytes)
-        launches = sum(1 for b in per_step_bytes if b > 0)
     else:
         # One event pair brackets the whole timed window on the launch
         # stream: markers between steps would add packets to the stream.
@@ -542,8 +543,7 @@ def main():
             "mean_kernel_us": round(mean_kernel_ms * 1e3, 2),
             "launches_timed": launches,
             "kernel_time": "GPU span of the timed window (one HIP event pair on the launch "
-                           "stream) / steps with work in it (a step the library splits into two "
-                           "kernels counts once)",
+                           "stream) / kernel launches in it",
         },
         "cpu_baseline": cpu,
     }

@@ -71,6 +71,11 @@ enum { RIP_FP32 = 0, RIP_BF16 = 1 };
 /* Message describing the last error on the calling thread ("" if none). */
 const char* rip_last_error(void);
 int32_t rip_abi_version(void);
+/* Kernel launches the calling thread's last rip_preduce, rip_local_step or
+ * rip_step enqueued: 0 (an error before any launch, or a step with no work),
+ * 1, or 2 (a step split by residency preference; see rip_preduce).  For
+ * accounting and tests; results never depend on it. */
+int32_t rip_last_launch_count(void);
 
 /* ------------------------------------------------------------------------
  * Group generation (Step 3 of Fig. 4; Sec. 4 and Sec. 5.1-5.3)

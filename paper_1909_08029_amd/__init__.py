@@ -88,6 +88,7 @@ def _load():
     sigs = {
         "rip_last_error": (ctypes.c_char_p, []),
         "rip_abi_version": (ctypes.c_int32, []),
+        "rip_last_launch_count": (ctypes.c_int32, []),
         "rip_sched_create": (ctypes.c_int32, [ctypes.POINTER(SchedCfg), ctypes.POINTER(vp)]),
         "rip_sched_destroy": (None, [vp]),
         "rip_schedule_groups": (ctypes.c_int32, [vp, ctypes.c_int64, ctypes.c_char_p, _i32p,
@@ -325,3 +326,8 @@ def rip_set_blocks_per_cu(n: int) -> None:
 
 def abi_version() -> int:
     return lib.rip_abi_version()
+
+
+def rip_last_launch_count() -> int:
+    """Kernel launches the calling thread's last step call enqueued (0-2)."""
+    return lib.rip_last_launch_count()

@@ -22,6 +22,7 @@ namespace rip {
 
 namespace {
 thread_local std::string g_last_error;
+thread_local int32_t g_last_launches = 0;  // kernels the last step call enqueued
 std::atomic<int> g_max_blocks{0};
 std::atomic<int> g_blocks_per_cu{0};
 // One workgroup per tile up to 2^25 workgroups (2^31 work-items, within the
@@ -93,6 +94,7 @@ int32_t fixed_array(int device, void** out) {
 }  // namespace rip
 
 extern "C" const char* rip_last_error(void) { return rip::g_last_error.c_str(); }
+extern "C" int32_t rip_last_launch_count(void) { return rip::g_last_launches; }
 extern "C" int32_t rip_abi_version(void) { return RIP_ABI_VERSION; }
 
 extern "C" int32_t rip_set_blocks_per_cu(int32_t blocks_per_cu) {
@@ -547,6 +549,7 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
                                const int32_t* members, int32_t n_groups, const int32_t* active,
                                int32_t n_active, const rip_sgd* sgd, void* stream) {
   rip::clear_error();
+  rip::g_last_launches = 0;
   if (!r) return rip::fail(RIP_E_INVAL, "rip_preduce: replicas handle is NULL");
   rip::StepArgs a;
   bool mom = false;
@@ -575,6 +578,7 @@ extern "C" int32_t rip_preduce(const rip_replicas* r, const int32_t* group_offse
     const hipError_t le = rip::launch_fused_step(x, r->dtype == RIP_BF16, mom, ext, blocks, lds,
                                                  static_cast<hipStream_t>(stream));
     if (le != hipSuccess) return rip::fail(RIP_E_HIP, "kernel launch: %s", hipGetErrorString(le));
+    ++rip::g_last_launches;
     return RIP_OK;
   };
   // One launch, or two when the units want residency caps far apart (and
@@ -597,6 +601,7 @@ extern "C" int32_t rip_step(rip_sched* s, const rip_replicas* r, int64_t step,
                             int32_t* active, int32_t* n_active, int32_t* group_offsets,
                             int32_t* members, int32_t* n_groups) {
   rip::clear_error();
+  rip::g_last_launches = 0;
   if (!s || !r || !sgd) return rip::fail(RIP_E_INVAL, "rip_step: null scheduler, replicas or sgd");
   if (rip::sched_workers(s) != r->n)
     return rip::fail(RIP_E_INVAL, "scheduler has %d workers, replicas handle %d",
@@ -634,6 +639,7 @@ extern "C" int32_t rip_local_step(const rip_replicas* r, const int32_t* active, 
                                   const rip_sgd* sgd, void* stream) {
   if (!sgd) {
     rip::clear_error();
+    rip::g_last_launches = 0;
     return rip::fail(RIP_E_INVAL, "rip_local_step: sgd is NULL");
   }
   return rip_preduce(r, nullptr, nullptr, 0, active, n_active, sgd, stream);

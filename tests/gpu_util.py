@@ -88,6 +88,7 @@ class DeviceRun:
                         for gs in self.state.grad_sets]
         self.sched = rip_scheduler(w)
         self.schedule: List[Tuple[List[int], List[Tuple[int, ...]]]] = []
+        self.launches: List[int] = []   # kernels each step enqueued
         self.t = 0
 
     def step(self):
@@ -98,11 +99,16 @@ class DeviceRun:
         opt = dict(weight_decay=w.weight_decay, nesterov=w.nesterov)
         if self.fused:
             rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, **opt)
+            kernels = rip.rip_last_launch_count()
         else:
+            kernels = 0
             if active:
                 rip.rip_local_step(h, active, w.lr, w.momentum, **opt)
+                kernels = rip.rip_last_launch_count()
             rip.rip_preduce(h, groups)
+            kernels += rip.rip_last_launch_count()
         self.schedule.append((active, groups))
+        self.launches.append(kernels)
         self.t += 1
 
     def run(self, steps: int):

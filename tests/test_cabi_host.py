@@ -161,8 +161,10 @@ def test_replicas_create_checks_before_any_device_call():
         rip.RIP_E_INVAL
     assert b"NULL" in lib.rip_last_error()
     assert lib.rip_preduce(None, None, None, 0, None, 0, None, None) == rip.RIP_E_INVAL
+    assert rip.rip_last_launch_count() == 0
     sgd = rip.Sgd(0.1, 0.0, 0.0, 0)
     assert lib.rip_local_step(None, None, 0, ctypes.byref(sgd), None) == rip.RIP_E_INVAL
+    assert rip.rip_last_launch_count() == 0
 
 
 def test_step_rejects_null_handles_and_leaves_the_scheduler():

@@ -44,12 +44,13 @@ def test_graph_replays_match_oracle(name, w):
     stats = dict(steps=0, updates=0, groups=0, members=0, empty=0)
     args = argparse.Namespace(steps=8, unfused=False)
     torch.cuda.synchronize()
-    L, per_step, span_ms, _ = bench.graph_steps(args, w, rip, handles, sched, 0,
-                                                torch.cuda.current_stream(), stats)
+    L, per_step, span_ms, _, kernels = bench.graph_steps(args, w, rip, handles, sched, 0,
+                                                         torch.cuda.current_stream(), stats)
     torch.cuda.synchronize()
     log(f"case graph {name}: period {L}, {args.steps} timed steps")
     assert len(per_step) == args.steps and stats["steps"] == args.steps
     assert span_ms > 0
+    assert kernels >= sum(1 for b in per_step if b > 0)
     total = sum(per_step)
     # one untimed replay, then steps / L timed ones: the schedule of steps 0 .. L + steps - 1
     ref = rip.Scheduler(w.n, dict(w.sched)["mode"],

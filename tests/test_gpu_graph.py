@@ -39,6 +39,8 @@ def _workload(dtype, momentum):
 def _launch_all(rip, h, w, stream):
     for active, groups in STEPS:
         rip.rip_preduce(h, groups, active, lr=w.lr, momentum=w.momentum, stream=stream)
+        # the last step is the one the library splits into two launches
+        assert rip.rip_last_launch_count() == (2 if len(groups[0]) == 8 else 1)
 
 
 def _state(st, w):

@@ -204,6 +204,23 @@ def test_other_schedulers_small(mode, kw):
     check_against_oracle(run, full_windows(w.numel), f"mode{mode}")
 
 
+@pytest.mark.parametrize("dtype,mom", [(DTYPE_F32, 0.9), (DTYPE_F32, 0.0), (DTYPE_BF16, 0.9)])
+def test_split_launches_global_division(dtype, mom):
+    """Global Division with groups of two to eight: steps whose units want
+    residency caps far apart run as two launches (checked through the launch
+    count the library reports); every element matches the oracle."""
+    n = 16
+    w = wl.scaled(wl.WORKLOADS[4], [3 * 4096 + 77], steps=16, n=n, dtype=dtype, momentum=mom,
+                  lr=0.1 if dtype == DTYPE_F32 else 20.0,
+                  param_sigma=1.0 if dtype == DTYPE_F32 else 0.05,
+                  sched=dict(mode=wl.GD, seed=12, kmin=2, kmax=8))
+    log(f"case split launches dtype={dtype} momentum={mom}")
+    run = DeviceRun(w)
+    run.run(w.steps)
+    assert 2 in run.launches and 1 in run.launches, run.launches
+    check_against_oracle(run, full_windows(w.numel), f"split dtype={dtype} mom={mom}")
+
+
 def test_allreduce_and_max_replicas():
     """k = N = 256 (the largest handle): P-Reduce over every replica is the
     global mean; then pairs (AD-PSGD's k = 2)."""
